@@ -1,0 +1,37 @@
+"""Plain fp64 CPU oracle for the token-aware verifier hot path.
+
+TEST INFRASTRUCTURE ONLY. Nothing in the product path may import this
+package: only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline
+leg of ``bench.py`` use it. It shares no code with the HIP library.
+
+The oracle writes out, in float64 and in the order the paper states them,
+what the verifier computes (Pro-Router, Sec. 3.1, eq:features and the
+ship rule p >= tau):
+
+* :mod:`oracle.features` -- per-token confidence features of one
+  vocabulary logit row after temperature and optional top-p.
+* :mod:`oracle.aggregate` -- per-request aggregation of those features
+  over a ragged batch, the summary score and the ship-or-escalate rule.
+
+Parity pinning: every function here is pinned by ``tests/test_oracle_pins.py``
+against closed forms, invariants and pure-Python brute force, except the
+default score head (a fixed linear summary chosen because the paper
+publishes no trained head weights), which is *parity unpinned* against the
+paper.
+"""
+
+from .features import (  # noqa: F401
+    FLAG_BAD_ID,
+    FLAG_BAD_TP,
+    FLAG_NONFINITE,
+    FLAG_OUTSIDE_NUCLEUS,
+    decode_logits,
+    token_features,
+    token_features_batch,
+)
+from .aggregate import (  # noqa: F401
+    AGG_FEATURES,
+    request_aggregate,
+    route,
+    score_from_aggregates,
+)
