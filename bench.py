@@ -1,0 +1,226 @@
+#!/usr/bin/env python3
+"""Throughput of the token-aware verifier hot path on one MI355X.
+
+A step is one pass of the whole offline path over one batch: per-token
+features of every logit row (pr_token_features), per-request summaries and
+score (pr_request_aggregate) and the ship decision (pr_route). The default
+workload is the ragged batch of 64 requests with lengths U{16..512}
+(about 16.9k rows) of V = 151,936 bfloat16 logits at T = 0.7; inputs are
+generated on the GPU before timing and stay resident in HBM.
+
+Prints one JSON line: rows/s (value), the row kernel's achieved HBM GB/s
+against the 8 TB/s peak (roofline, from HIP events around each launch in
+the timed region) and the fp64 oracle's rows/s on the host (cpu_baseline,
+a bounded sample), plus a parity spot check of that sample.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBS = 8000.0
+
+
+def parse_args():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="ragged_64req_v151936_bf16")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="time budget of the oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also time a plain device copy of known size (HBM counter calibration)")
+    ap.add_argument("--traffic-json", default=os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                           "profiles", "traffic.json"))
+    return ap.parse_args()
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes_per_row(V: int, elem_bytes: int) -> int:
+    # one read of the logit row + sampled id and temperature in + 10 outputs of 4 bytes
+    return V * elem_bytes + 4 + 4 + 10 * 4
+
+
+def copy_probe(torch, nbytes=1 << 30, reps=10):
+    src = torch.empty(nbytes // 4, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    return {"bytes_read": nbytes, "bytes_written": nbytes, "ms": ms, "gb_per_s": 2 * nbytes / ms / 1e6}
+
+
+def cpu_baseline(torch, batch, feats_gpu, seconds):
+    """The fp64 oracle on the first rows of the batch, time-bounded, one core."""
+    import oracle
+    from oracle import aggregate as oagg
+    from paper_2608_28726_amd import workloads as wl
+    w = batch.workload
+    n_max = min(batch.n_rows, 4096)
+    raw = wl.to_host_raw(batch.logits[:n_max])
+    ids = batch.sampled_ids[:n_max].cpu().numpy()
+    T = batch.temperature[:n_max].cpu().numpy()
+    P = None if batch.top_p is None else batch.top_p[:n_max].cpu().numpy()
+    dtype = "bf16" if w.dtype == "bf16" else "f32"
+    res = []
+    t0 = time.perf_counter()
+    while len(res) < n_max and (len(res) < 16 or time.perf_counter() - t0 < seconds):
+        r = len(res)
+        res.append(oracle.token_features(raw[r], dtype, int(ids[r]), float(T[r]), None if P is None else float(P[r])))
+    n = len(res)
+    # whole requests inside the sample are also aggregated, scored and routed
+    offs = batch.offsets
+    n_whole = int(np.searchsorted(offs, n, side="right")) - 1
+    of = {k: np.array([d[k] for d in res]) for k in ("logprob", "maxprob", "entropy", "margin")}
+    if n_whole > 0:
+        agg = oagg.request_aggregate(of, offs[: n_whole + 1], q=w.q)
+        oagg.route(oagg.score_from_aggregates(agg), w.tau)
+    elapsed = time.perf_counter() - t0
+    # parity spot check of the sample against the GPU's features
+    bad = 0
+    for k in ("max_logit", "lse", "entropy", "logprob", "maxprob", "margin"):
+        g = feats_gpu[k][:n].cpu().numpy().astype(np.float64)
+        o = np.array([d[k] for d in res])
+        ok = (np.abs(g - o) <= 1e-5 + 1e-4 * np.abs(o)) | (np.isnan(g) & np.isnan(o)) | (g == o)
+        bad += int((~ok).sum())
+    for k in ("rank", "argmax", "cutoff"):
+        bad += int((feats_gpu[k][:n].cpu().numpy() != np.array([d[k] for d in res])).sum())
+    cores = 1
+    return {
+        "value": n / elapsed,
+        "unit": "rows/s",
+        "cores": cores,
+        "kind": "oracle",
+        "sample": f"first {n} rows ({n_whole} whole requests) of the same batch: all per-token features in "
+                  f"float64, plus summaries, score and route of the whole requests; {elapsed:.1f} s on "
+                  f"{cores} host core (numpy, single-threaded)",
+        "parity_mismatches": bad,
+        "rows": n,
+    }
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported by this build "
+              "(rows and requests are independent: see the sharding paragraph of the design notes).",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_2608_28726_amd as pr
+    from paper_2608_28726_amd import workloads as wl
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+
+    w = wl.WORKLOADS[args.workload]
+    log(f"[bench] generating {w.name} on the GPU")
+    batch = wl.make_batch(w, device="cuda")
+    n_rows = batch.n_rows
+    offsets = torch.as_tensor(batch.offsets).cuda()
+    torch.cuda.synchronize()
+    log(f"[bench] rows={n_rows} V={w.V} dtype={w.dtype} bytes={n_rows * w.V * w.elem_bytes / 1e9:.2f} GB")
+
+    feats = pr.token_features(batch.logits, batch.sampled_ids, batch.temperature, batch.top_p)
+    ws_bytes = pr.token_features_workspace(batch.logits, batch.top_p is not None)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device="cuda")
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record()
+        pr.token_features(batch.logits, batch.sampled_ids, batch.temperature, batch.top_p, out=feats, workspace=ws)
+        if ev is not None:
+            ev[1].record()
+        agg = pr.request_aggregate(feats, offsets, q=w.q)
+        return pr.route(agg["score"], w.tau)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+    log(f"[bench] timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        ship, n_ship = step(events[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kern_ms = [a.elapsed_time(b) for a, b in events]
+    avg_ms = float(np.mean(kern_ms))
+    ms_per_step = elapsed * 1e3 / args.steps
+    rows_per_s = n_rows * args.steps / elapsed
+    bytes_launch = n_rows * algorithmic_bytes_per_row(w.V, w.elem_bytes)
+    achieved = bytes_launch / (avg_ms * 1e-3) / 1e9
+    log(f"[bench] {ms_per_step:.3f} ms/step, row kernel {avg_ms:.3f} ms ({achieved:.0f} GB/s), "
+        f"n_ship={int(n_ship.item())}/{w.n_req}")
+
+    traffic = None
+    if os.path.exists(args.traffic_json):
+        try:
+            t = json.load(open(args.traffic_json)).get(w.name)
+            if t and t.get("kernel_source_hash") == kernel_source_hash():
+                traffic = t["bytes_per_launch"]
+        except (OSError, ValueError):
+            traffic = None
+
+    result = {
+        "metric": "verified token rows/sec and achieved HBM GB/s (% of peak), V=151,936 bf16",
+        "value": rows_per_s,
+        "unit": "rows/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "n_req": w.n_req, "rows": n_rows, "V": w.V, "logits": w.dtype,
+                   "temperature": [w.T_lo, w.T_hi], "top_p": None if w.P_lo is None else [w.P_lo, w.P_hi],
+                   "aggregation": f"mean/min/q={w.q} nearest-rank", "threshold": w.tau},
+        "gb_per_s": achieved,
+        "pct_of_hbm_peak": 100.0 * achieved / HBM_PEAK_GBS,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                     "kernel": "row_features_kernel", "kernel_ms": avg_ms, "bytes_per_launch": bytes_launch},
+    }
+    if args.copy_probe:
+        result["copy_probe"] = copy_probe(torch)
+    if not args.no_cpu_baseline:
+        log("[bench] timing the oracle on the host")
+        result["cpu_baseline"] = cpu_baseline(torch, batch, feats, args.cpu_seconds)
+        log(f"[bench] oracle {result['cpu_baseline']['value']:.1f} rows/s, "
+            f"parity mismatches {result['cpu_baseline']['parity_mismatches']}")
+    print(json.dumps(result), flush=True)
+
+
+def kernel_source_hash() -> str:
+    """Hash of the kernel sources: stored counter traffic is only valid for the same kernels."""
+    import hashlib
+    d = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_28726_amd", "csrc")
+    h = hashlib.sha256()
+    for fn in sorted(os.listdir(d)):
+        if fn.endswith((".hip", ".h")):
+            h.update(open(os.path.join(d, fn), "rb").read())
+    return h.hexdigest()[:16]
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,228 @@
+/*
+ * prouter.h -- C ABI of the token-aware verifier hot path for MI355X (gfx950).
+ *
+ * The library turns each generated token's vocabulary logit row into
+ * confidence features, summarises them per request and decides per request
+ * whether the small model's answer ships or escalates (Pro-Router, Sec. 3.1:
+ * per-token features, Eq. 3; the ship rule p >= tau stated with the gain,
+ * Eq. 1; the quantile-summary verifier input, Sec. 4.2, Table "ablation").
+ *
+ * Conventions for every call:
+ *  - Data pointers are DEVICE pointers unless a comment says otherwise. The
+ *    caller owns all memory; the library never frees caller memory.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    Calls only enqueue work on it and return; nothing synchronises the
+ *    stream except pr_validate_offsets, which says so.
+ *  - Errors in host-visible arguments (NULL required pointer, bad sizes,
+ *    misalignment, unknown enum) return PR_ERR_INVALID_ARG and launch
+ *    nothing. Errors in device data (NaN logits, bad ids, bad temperature)
+ *    cannot be seen without a sync: they set per-row flags and the call
+ *    still returns PR_OK. A failed launch returns PR_ERR_HIP.
+ *  - No C++ exception crosses this boundary.
+ */
+#ifndef PROUTER_H
+#define PROUTER_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum pr_status {
+  PR_OK = 0,
+  PR_ERR_INVALID_ARG = 1,
+  PR_ERR_UNSUPPORTED = 2,
+  PR_ERR_HIP = 3,
+  PR_ERR_NO_MEMORY = 4
+} pr_status;
+
+/* Storage type of the logits. bf16 is the upper 16 bits of an IEEE float32. */
+typedef enum pr_dtype { PR_F32 = 0, PR_BF16 = 1 } pr_dtype;
+
+/* Per-row flags (bit set in pr_token_features_t.flags). */
+#define PR_FLAG_NONFINITE 1u       /* a NaN or +inf logit, or every logit is -inf; all float
+                                      outputs NaN, all integer outputs -1                     */
+#define PR_FLAG_BAD_ID 2u          /* sampled id outside [0, V): logprob NaN, rank -1; the
+                                      other outputs are still valid                           */
+#define PR_FLAG_BAD_TP 4u          /* temperature not finite or <= 0, top-p NaN or <= 0, or
+                                      |max logit| > 2^100 * T; outputs as for NONFINITE       */
+#define PR_FLAG_OUTSIDE_NUCLEUS 8u /* top-p on and the sampled token lies outside the
+                                      nucleus: logprob = -inf, rank > cutoff                  */
+
+/*
+ * Per-token outputs, one array per feature, each [n_rows] (structure of
+ * arrays). Definitions (u = z / T, order of tokens: larger raw logit first,
+ * equal logits by lower index; N = the nucleus, all V tokens when top-p is off):
+ *   max_logit  z_argmax / T
+ *   lse        log sum_{v in N} exp(u_v)                  (nucleus normaliser)
+ *   entropy    Shannon entropy in nats of softmax(u) renormalised on N
+ *   logprob    log p_N(y), -inf if y is outside N          (Eq. 3, l_t)
+ *   maxprob    max_v p_N(v)                                (Eq. 3, m_t)
+ *   margin     (z_argmax - z_second) / T, over all tokens
+ *   rank       1-based position of y in the order
+ *   argmax     first token of the order
+ *   cutoff     |N| (V when top-p is off)
+ *   flags      PR_FLAG_* bits
+ */
+typedef struct pr_token_features_t {
+  float* max_logit;
+  float* lse;
+  float* entropy;
+  float* logprob;
+  float* maxprob;
+  float* margin;
+  int32_t* rank;
+  int32_t* argmax;
+  int32_t* cutoff;
+  uint32_t* flags;
+} pr_token_features_t;
+
+/*
+ * Summary head. The summarised per-token tuple is
+ *   A = (logprob, maxprob, -entropy, margin)        (feature index f = 0..3)
+ * (the entropy is negated as the paper's h_t = -H_t so that every column
+ * rises with confidence). Statistics (index s): 0 mean, 1 min, 2 the
+ * nearest-rank q-quantile, i.e. the j-th smallest value with
+ * j = max(1, ceil(q * n)), q * n rounded once in double.
+ * score = link(b + sum over w[s*4+f] != 0 of w[s*4+f] * stat_s(A_f)),
+ * link 0 = identity, 1 = logistic sigmoid. Zero weights are skipped.
+ * Defaults (pr_agg_params_default): q = 0.1, w = 1 on mean(maxprob) only,
+ * b = 0, identity -- the score is the request's mean max-probability.
+ */
+typedef struct pr_agg_params {
+  double q;
+  double w[12];
+  double b;
+  int32_t link;
+} pr_agg_params;
+
+/* Per-request outputs. mean/min/quant are [n_req][4] (row-major, feature
+ * index fastest); count and score are [n_req]. Any member may be NULL when
+ * that output is not wanted (score is needed by pr_route). An empty request
+ * or a NaN value in a feature's segment gives NaN summaries (and score). */
+typedef struct pr_request_agg_t {
+  int32_t* count;
+  float* mean;
+  float* min;
+  float* quant;
+  float* score;
+} pr_request_agg_t;
+
+/* Human-readable name of a status code (static string, host). */
+const char* pr_status_string(pr_status status);
+
+/* Fills *params (host pointer) with the default summary head. */
+void pr_agg_params_default(pr_agg_params* params);
+
+/*
+ * Bytes of device workspace pr_token_features needs for this shape (0 when
+ * none). top_p_on: 1 if a top-p array will be passed.
+ */
+size_t pr_token_features_workspace(pr_dtype dtype, int64_t n_rows, int32_t vocab, int32_t top_p_on);
+
+/*
+ * Per-token features of n_rows logit rows (Sec. 3.1, Eq. 3, extended to the
+ * feature set documented at pr_token_features_t; top-p as a nucleus prefix of
+ * the token order).
+ *   logits       [n_rows][row_stride] of dtype; row r starts at element
+ *                r * row_stride. Requires vocab >= 2, row_stride >= vocab and
+ *                the base aligned to the element size.
+ *   sampled_ids  int32 [n_rows], the emitted token of each row.
+ *   temperature  float [n_rows], per-row temperature (> 0).
+ *   top_p        float [n_rows] or NULL (off). P >= 1 switches a row's
+ *                truncation off; 0 < P < 1 keeps the shortest prefix of the
+ *                order whose mass reaches P of the total.
+ *   out          host pointer to a struct of device output arrays, all
+ *                required.
+ *   workspace    device scratch of at least
+ *                pr_token_features_workspace(...) bytes (may be NULL when that
+ *                is 0). Its contents need no initialisation.
+ * n_rows == 0 is valid and launches nothing.
+ */
+pr_status pr_token_features(const void* logits, pr_dtype dtype, int64_t n_rows, int32_t vocab,
+                            int64_t row_stride, const int32_t* sampled_ids, const float* temperature,
+                            const float* top_p, const pr_token_features_t* out, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
+/*
+ * Ragged per-request summaries and score (Sec. 3.1, the stacked feature
+ * sequence X; Sec. 4.2, Table "ablation", quantile-summary input).
+ *   feats     host pointer to the per-token arrays; logprob, maxprob, entropy
+ *             and margin are read.
+ *   offsets   int32 [n_req + 1], device. Request i owns rows
+ *             offsets[i] .. offsets[i+1]-1. Precondition (not checked here,
+ *             see pr_validate_offsets): offsets[0] >= 0, non-decreasing.
+ *   params    host pointer, or NULL for the defaults.
+ *   out       host pointer to a struct of device output arrays.
+ */
+pr_status pr_request_aggregate(const pr_token_features_t* feats, const int32_t* offsets, int32_t n_req,
+                               const pr_agg_params* params, const pr_request_agg_t* out, void* stream);
+
+/*
+ * Ship-or-escalate (Sec. 3.1: ship iff p >= tau). ship[i] = 1 iff
+ * scores[i] >= threshold; a NaN score escalates (0). n_ship, if not NULL,
+ * receives the number of shipped requests (device int32).
+ */
+pr_status pr_route(const float* scores, int32_t n_req, float threshold, uint8_t* ship, int32_t* n_ship,
+                   void* stream);
+
+/*
+ * Synchronous debug check of an offsets array (device pointer): returns
+ * PR_OK iff offsets[0] == 0, offsets are non-decreasing and
+ * offsets[n_req] == n_rows. Synchronises `stream`.
+ */
+pr_status pr_validate_offsets(const int32_t* offsets, int32_t n_req, int64_t n_rows, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Streaming decode-step variant. Per-request state stays on the device
+ * between steps; a request's verdict is taken when it finishes, as the
+ * paper's verifier decides when the engine reports a request finished
+ * (Sec. 4.1, implementation details).
+ * ------------------------------------------------------------------------ */
+typedef struct pr_stream pr_stream;
+
+/*
+ * Allocates the device state for max_slots concurrent requests of at most
+ * max_len tokens each, on the current device (the only allocating call of
+ * the streaming API). params may be NULL (defaults). *state is a host handle.
+ */
+pr_status pr_stream_create(int32_t max_slots, int32_t max_len, const pr_agg_params* params, pr_stream** state);
+
+/*
+ * One decode step: features of n_active rows (same layout and rules as
+ * pr_token_features), and for each row r the slot slot_ids[r] (device
+ * int32 [n_active]) gains one token: count, running sums and minima of A,
+ * and the token's A is appended to the slot's history (needed for the exact
+ * quantile). A slot may appear at most once per step (duplicates race).
+ * Tokens past max_len are counted in sums and minima but not kept, and the
+ * slot's quantile becomes NaN. out may be NULL (features not returned).
+ * top_p must be NULL (PR_ERR_UNSUPPORTED otherwise).
+ */
+pr_status pr_stream_step(pr_stream* state, const void* logits, pr_dtype dtype, int32_t n_active,
+                         int32_t vocab, int64_t row_stride, const int32_t* slot_ids,
+                         const int32_t* sampled_ids, const float* temperature, const float* top_p,
+                         const pr_token_features_t* out, void* stream);
+
+/*
+ * Finishes n requests: for each slots[i] (device int32 [n]) computes the
+ * summaries and score as pr_request_aggregate would over the slot's tokens,
+ * writes them to out[i] (members may be NULL; the struct pointer is a host
+ * pointer), sets ship[i] (device uint8 [n], may be NULL) by
+ * score >= threshold, then clears the slot for reuse.
+ */
+pr_status pr_stream_finish(pr_stream* state, const int32_t* slots, int32_t n, float threshold,
+                           const pr_request_agg_t* out, uint8_t* ship, void* stream);
+
+/* Clears n slots (device int32 [n]) without producing a verdict. */
+pr_status pr_stream_reset_slots(pr_stream* state, const int32_t* slots, int32_t n, void* stream);
+
+/* Frees the state (synchronises the device first). NULL is ignored. */
+void pr_stream_destroy(pr_stream* state);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PROUTER_H */

@@ -32,7 +32,8 @@ R5  Entropy is in nats; 0 * log 0 counts as 0.
 R6  margin = (z_argmax - z_second) / T in scaled-logit space over the full
     order (a tie gives 0; top-p does not change it).
 R7  A row with a bad sampled id still gets every feature that does not depend
-    on the id; log-probability is NaN and rank is -1.
+    on the id; log-probability is NaN and rank is -1. The bad-id flag is set
+    whenever the id is out of range, also on rows flagged for other reasons.
 """
 
 from __future__ import annotations
@@ -95,14 +96,15 @@ def token_features(raw_row, dtype: str, y: int, T: float, P: float | None = None
     T = float(np.float32(T))
     P = None if P is None else float(np.float32(P))
 
-    flags = 0
+    bad_id = not (0 <= y < V)
+    flags = FLAG_BAD_ID if bad_id else 0  # R7: a bad id is reported in every case
     if np.isnan(z).any() or np.isposinf(z).any() or np.isneginf(z).all():
         flags |= FLAG_NONFINITE
     if not (math.isfinite(T) and T > 0.0):
         flags |= FLAG_BAD_TP
     if P is not None and (math.isnan(P) or P <= 0.0):
         flags |= FLAG_BAD_TP
-    if flags:
+    if flags & (FLAG_NONFINITE | FLAG_BAD_TP):
         return _nan_result(V, flags)
 
     # R2: the order. argmax is the lowest index holding the largest value.
@@ -110,12 +112,10 @@ def token_features(raw_row, dtype: str, y: int, T: float, P: float | None = None
     z_max = z.max()
     a = int(np.flatnonzero(z == z_max)[0])
     if abs(z[a]) > T * _TEMP_RANGE:  # exact: scaling by 2**100 does not round
-        return _nan_result(V, FLAG_BAD_TP)
+        return _nan_result(V, flags | FLAG_BAD_TP)
     z_second = np.delete(z, a).max()
 
-    bad_id = not (0 <= y < V)
     if bad_id:
-        flags |= FLAG_BAD_ID
         rank = -1
     else:
         rank = 1 + int(np.count_nonzero(z > z[y])) + int(np.count_nonzero((z == z[y]) & (idx < y)))
@@ -164,7 +164,9 @@ def token_features(raw_row, dtype: str, y: int, T: float, P: float | None = None
     if bad_id:
         logprob = math.nan
     elif rank <= k:
-        logprob = u[y] - lse if e[y] > 0.0 else -math.inf
+        # log p(y) = u_y - lse: finite even where p(y) underflows float64;
+        # -inf only for a masked logit (u_y = -inf).
+        logprob = u[y] - lse
     else:
         logprob = -math.inf
         flags |= FLAG_OUTSIDE_NUCLEUS

@@ -1,0 +1,221 @@
+"""Token-aware verifier hot path on MI355X (Pro-Router, Sec. 3.1).
+
+A thin binding over the C ABI of ``libprouter.so`` (include/prouter.h):
+tensors are checked and their device pointers handed to the library, which
+runs every step of the path in its own HIP kernels on torch's current
+stream. PyTorch only provides device memory and streams here.
+
+    feats = token_features(logits, sampled_ids, temperature, top_p=None)
+    agg = request_aggregate(feats, offsets)
+    ship, n_ship = route(agg["score"], threshold)
+
+Streaming decode: :class:`StreamState`.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+
+import torch
+
+from . import _abi
+from ._abi import (FLAG_BAD_ID, FLAG_BAD_TP, FLAG_NONFINITE, FLAG_OUTSIDE_NUCLEUS,  # noqa: F401
+                   ProuterError)
+
+__all__ = ["token_features", "request_aggregate", "route", "validate_offsets", "StreamState",
+           "token_features_workspace", "ProuterError", "FEATURE_FLOATS", "FEATURE_INTS"]
+
+FEATURE_FLOATS = ("max_logit", "lse", "entropy", "logprob", "maxprob", "margin")
+FEATURE_INTS = ("rank", "argmax", "cutoff")
+_LINKS = {"identity": 0, "sigmoid": 1}
+
+
+def _stream_handle() -> C.c_void_p:
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _ptr(t) -> C.c_void_p | None:
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _dtype_code(logits: torch.Tensor) -> int:
+    if logits.dtype == torch.float32:
+        return _abi.PR_F32
+    if logits.dtype == torch.bfloat16:
+        return _abi.PR_BF16
+    raise TypeError(f"logits must be float32 or bfloat16, got {logits.dtype}")
+
+
+def _check_rows(logits, sampled_ids, temperature, top_p):
+    if not logits.is_cuda or logits.dim() != 2 or logits.stride(1) != 1:
+        raise ValueError("logits must be a 2-D CUDA tensor with unit stride along the vocabulary")
+    n = logits.shape[0]
+    for name, t, dt in (("sampled_ids", sampled_ids, torch.int32), ("temperature", temperature, torch.float32),
+                        ("top_p", top_p, torch.float32)):
+        if t is None:
+            continue
+        if t.dtype != dt or not t.is_cuda or t.dim() != 1 or t.shape[0] != n or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous 1-D {dt} CUDA tensor of length {n}")
+
+
+def _as_row_tensor(x, n, device):
+    if isinstance(x, (int, float)):
+        return torch.full((n,), float(x), dtype=torch.float32, device=device)
+    return x
+
+
+def _alloc_features(n: int, device) -> dict:
+    out = {k: torch.empty(n, dtype=torch.float32, device=device) for k in FEATURE_FLOATS}
+    out.update({k: torch.empty(n, dtype=torch.int32, device=device) for k in FEATURE_INTS})
+    out["flags"] = torch.empty(n, dtype=torch.int32, device=device)  # uint32 bits
+    return out
+
+
+def _features_struct(f: dict) -> _abi.TokenFeatures:
+    return _abi.TokenFeatures(*[f[k].data_ptr() if f.get(k) is not None else None for k in _abi.FEATURE_FIELDS])
+
+
+def token_features_workspace(logits: torch.Tensor, top_p_on: bool = False) -> int:
+    n, V = logits.shape
+    return int(_abi.lib().pr_token_features_workspace(_dtype_code(logits), n, V, int(top_p_on)))
+
+
+def token_features(logits: torch.Tensor, sampled_ids: torch.Tensor, temperature, top_p=None,
+                   out: dict | None = None, workspace: torch.Tensor | None = None) -> dict:
+    """Per-token features of each logit row (``pr_token_features``).
+
+    ``logits`` [n_rows, V] float32/bfloat16; ``sampled_ids`` int32 [n_rows];
+    ``temperature`` float32 [n_rows] or a Python float; ``top_p`` float32
+    [n_rows], a Python float or None. Returns a dict of [n_rows] tensors.
+    """
+    n, V = logits.shape
+    temperature = _as_row_tensor(temperature, n, logits.device)
+    top_p = None if top_p is None else _as_row_tensor(top_p, n, logits.device)
+    _check_rows(logits, sampled_ids, temperature, top_p)
+    L = _abi.lib()
+    code = _dtype_code(logits)
+    out = _alloc_features(n, logits.device) if out is None else out
+    need = int(L.pr_token_features_workspace(code, n, V, int(top_p is not None)))
+    if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
+        workspace = torch.empty(need, dtype=torch.uint8, device=logits.device)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    st = L.pr_token_features(_ptr(logits), code, n, V, logits.stride(0), _ptr(sampled_ids), _ptr(temperature),
+                             _ptr(top_p), C.byref(_features_struct(out)), _ptr(workspace), ws_bytes,
+                             _stream_handle())
+    _abi.check("pr_token_features", st)
+    return out
+
+
+def _params(q=0.1, weights=None, bias=0.0, link="identity") -> _abi.AggParams:
+    p = _abi.AggParams()
+    _abi.lib().pr_agg_params_default(C.byref(p))
+    p.q = float(q)
+    if weights is not None:
+        w = [float(v) for v in torch.as_tensor(weights, dtype=torch.float64).reshape(-1).tolist()]
+        if len(w) != 12:
+            raise ValueError("weights must have 12 entries (stat-major [mean, min, quant] x 4 features)")
+        for i, v in enumerate(w):
+            p.w[i] = v
+    p.b = float(bias)
+    p.link = _LINKS[link]
+    return p
+
+
+def _alloc_agg(n: int, device) -> dict:
+    return {"count": torch.empty(n, dtype=torch.int32, device=device),
+            "mean": torch.empty(n, 4, dtype=torch.float32, device=device),
+            "min": torch.empty(n, 4, dtype=torch.float32, device=device),
+            "quant": torch.empty(n, 4, dtype=torch.float32, device=device),
+            "score": torch.empty(n, dtype=torch.float32, device=device)}
+
+
+def _agg_struct(a: dict) -> _abi.RequestAgg:
+    return _abi.RequestAgg(*[a[k].data_ptr() if a.get(k) is not None else None for k in _abi.AGG_FIELDS])
+
+
+def request_aggregate(feats: dict, offsets: torch.Tensor, q: float = 0.1, weights=None, bias: float = 0.0,
+                      link: str = "identity") -> dict:
+    """Per-request count, mean/min/q-quantile of (logprob, maxprob, -entropy,
+    margin) and the summary score (``pr_request_aggregate``)."""
+    if offsets.dtype != torch.int32 or not offsets.is_cuda or offsets.dim() != 1 or not offsets.is_contiguous():
+        raise ValueError("offsets must be a contiguous 1-D int32 CUDA tensor")
+    n_req = offsets.shape[0] - 1
+    out = _alloc_agg(n_req, offsets.device)
+    params = _params(q, weights, bias, link)
+    st = _abi.lib().pr_request_aggregate(C.byref(_features_struct(feats)), _ptr(offsets), n_req, C.byref(params),
+                                         C.byref(_agg_struct(out)), _stream_handle())
+    _abi.check("pr_request_aggregate", st)
+    return out
+
+
+def route(scores: torch.Tensor, threshold: float):
+    """Ship iff score >= threshold (``pr_route``). Returns (ship uint8 [n], n_ship int32 [1])."""
+    if scores.dtype != torch.float32 or not scores.is_cuda or not scores.is_contiguous():
+        raise ValueError("scores must be a contiguous float32 CUDA tensor")
+    n = scores.shape[0]
+    ship = torch.empty(n, dtype=torch.uint8, device=scores.device)
+    n_ship = torch.empty(1, dtype=torch.int32, device=scores.device)
+    st = _abi.lib().pr_route(_ptr(scores), n, float(threshold), _ptr(ship), _ptr(n_ship), _stream_handle())
+    _abi.check("pr_route", st)
+    return ship, n_ship
+
+
+def validate_offsets(offsets: torch.Tensor, n_rows: int) -> bool:
+    """Synchronous check of an offsets array (``pr_validate_offsets``)."""
+    st = _abi.lib().pr_validate_offsets(_ptr(offsets), offsets.shape[0] - 1, n_rows, _stream_handle())
+    if st == _abi.PR_ERR_INVALID_ARG:
+        return False
+    _abi.check("pr_validate_offsets", st)
+    return True
+
+
+class StreamState:
+    """Device-resident per-request state for streaming decode (``pr_stream_*``)."""
+
+    def __init__(self, max_slots: int, max_len: int, q: float = 0.1, weights=None, bias: float = 0.0,
+                 link: str = "identity"):
+        self._h = C.c_void_p()
+        params = _params(q, weights, bias, link)
+        _abi.check("pr_stream_create", _abi.lib().pr_stream_create(max_slots, max_len, C.byref(params),
+                                                                     C.byref(self._h)))
+        self.max_slots, self.max_len = max_slots, max_len
+
+    def step(self, logits, slot_ids, sampled_ids, temperature, out: dict | None = None, want_features=False):
+        n, V = logits.shape
+        temperature = _as_row_tensor(temperature, n, logits.device)
+        _check_rows(logits, sampled_ids, temperature, None)
+        if slot_ids.dtype != torch.int32 or slot_ids.shape[0] != n:
+            raise ValueError("slot_ids must be int32 [n_active]")
+        if out is None and want_features:
+            out = _alloc_features(n, logits.device)
+        fs = C.byref(_features_struct(out)) if out is not None else None
+        st = _abi.lib().pr_stream_step(self._h, _ptr(logits), _dtype_code(logits), n, V, logits.stride(0),
+                                       _ptr(slot_ids), _ptr(sampled_ids), _ptr(temperature), None, fs,
+                                       _stream_handle())
+        _abi.check("pr_stream_step", st)
+        return out
+
+    def finish(self, slots: torch.Tensor, threshold: float) -> dict:
+        n = slots.shape[0]
+        out = _alloc_agg(n, slots.device)
+        ship = torch.empty(n, dtype=torch.uint8, device=slots.device)
+        st = _abi.lib().pr_stream_finish(self._h, _ptr(slots), n, float(threshold), C.byref(_agg_struct(out)),
+                                         _ptr(ship), _stream_handle())
+        _abi.check("pr_stream_finish", st)
+        out["ship"] = ship
+        return out
+
+    def reset(self, slots: torch.Tensor) -> None:
+        _abi.check("pr_stream_reset_slots",
+                   _abi.lib().pr_stream_reset_slots(self._h, _ptr(slots), slots.shape[0], _stream_handle()))
+
+    def close(self) -> None:
+        if self._h:
+            _abi.lib().pr_stream_destroy(self._h)
+            self._h = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

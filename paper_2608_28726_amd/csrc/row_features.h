@@ -1,0 +1,43 @@
+// Launch interface of the row-reduction and top-p kernels (internal).
+#pragma once
+
+#include "device_util.h"
+
+namespace pr {
+
+// Device-resident state of the streaming decode variant, one entry per slot.
+struct StreamDev {
+  int32_t max_slots;
+  int32_t max_len;
+  int32_t* count;     // [max_slots] tokens seen
+  uint32_t* nanbits;  // [max_slots] bit f set: a NaN value of feature f was seen
+  double* sum;        // [max_slots][4] running sums of A
+  float* minv;        // [max_slots][4] running minima of A (+inf when empty)
+  float* hist;        // [max_slots][4][max_len] every token's A, for the exact quantile
+};
+
+struct RowArgs {
+  const void* logits;
+  int64_t n_rows;
+  int32_t V;
+  int64_t row_stride;
+  const int32_t* sampled_ids;
+  const float* temperature;
+  const float* top_p;
+  pr_token_features_t out;  // max_logit == NULL: outputs not written (streaming only)
+  int G;                    // workgroups per row
+  Partial* ws;              // [n_rows][G] partial states when G > 1
+  uint32_t* counters;       // [n_rows] arrival counters (streaming, G > 1); zero between launches
+  const int32_t* slot_ids;  // streaming only
+  StreamDev st;             // streaming only
+};
+
+// Workgroups per row chosen for a shape (the same in every call, so that the
+// workspace size query and the launch agree).
+int row_split(int64_t n_rows, int32_t V, pr_dtype dtype);
+
+// mode 0: offline (one kernel when G == 1, partial + merge kernels otherwise);
+// mode 2: streaming step (merge in the last workgroup of each row).
+hipError_t launch_row_features(const RowArgs& a, pr_dtype dtype, int mode, hipStream_t stream);
+
+}  // namespace pr

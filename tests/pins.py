@@ -67,7 +67,7 @@ def brute_row(z, y, T, P=None):
     q = {v: p[v] / mass_N for v in N}
     entropy = -math.fsum(q[v] * math.log(q[v]) for v in N if q[v] > 0)
     lse = math.log(math.fsum(math.exp(z[v] / T) for v in N if z[v] != -math.inf))
-    logprob = math.log(q[y]) if (y in N and q[y] > 0) else -math.inf
+    logprob = (z[y] / T - lse) if (y in N and z[y] != -math.inf) else -math.inf
     return {
         "max_logit": z[a] / T,
         "lse": lse,
@@ -266,6 +266,17 @@ def pin_shift(tf):
     return fails
 
 
+def pin_underflow_logprob(tf):
+    """log p(y) stays finite when p(y) underflows float64: (z_y - z_a)/T - log S."""
+    z = np.array([0.0, -60.0, -2.0], dtype=F32)
+    T = 0.05  # p(1) = exp(-1200) / S underflows
+    T32 = float(F32(T))
+    S = 1.0 + math.exp(-40.0)  # exp(-1200) is below double's range
+    expect = (-60.0) / T32 - math.log(S)
+    r = tf(z, "f32", 1, T)
+    return [] if close(r["logprob"], expect, 1e-12) else [f"underflow logprob {r['logprob']} != {expect}"]
+
+
 def pin_permutation(tf):
     """Distinct values: permuting tokens (and y with them) permutes argmax only."""
     rng = np.random.default_rng(13)
@@ -288,7 +299,7 @@ def pin_permutation(tf):
 
 ALL_FEATURE_PINS = [pin_uniform, pin_one_hot, pin_two_token, pin_dyadic_topp, pin_tie_grid,
                     pin_topp_tie_grid, pin_brute_random, pin_power_of_two_temperature, pin_shift,
-                    pin_permutation]
+                    pin_permutation, pin_underflow_logprob]
 
 
 def pin_bf16_decode(tf):

@@ -1,0 +1,108 @@
+"""The C-ABI library loads, exports every declared symbol and checks its
+host-visible arguments (CPU only: no call here reaches the GPU)."""
+
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from tests.helpers import ROOT, ensure_built
+
+
+def declared_symbols():
+    names = set()
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", fn)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names |= set(re.findall(r"\b(pr_[a-z_0-9]+)\s*\(", src))
+    return sorted(names)
+
+
+def test_every_declared_symbol_is_exported():
+    lib = ensure_built()
+    names = declared_symbols()
+    assert "pr_token_features" in names and "pr_request_aggregate" in names and "pr_route" in names
+    missing = [n for n in names if not hasattr(lib, n)]
+    assert not missing, f"declared but not exported: {missing}"
+
+
+def test_binding_covers_exports():
+    from paper_2608_28726_amd import _abi
+    assert sorted(_abi.EXPORTED) == declared_symbols()
+
+
+def test_status_strings_and_defaults():
+    lib = ensure_built()
+    from paper_2608_28726_amd import _abi
+    assert lib.pr_status_string(0) == b"ok"
+    assert lib.pr_status_string(1) == b"invalid argument"
+    assert lib.pr_status_string(99) == b"unknown status"
+    p = _abi.AggParams()
+    lib.pr_agg_params_default(C.byref(p))
+    assert p.q == 0.1 and p.b == 0.0 and p.link == 0
+    assert list(p.w) == [0.0, 1.0] + [0.0] * 10
+
+
+def test_workspace_sizes():
+    lib = ensure_built()
+    # Many rows: one workgroup per row, no workspace.
+    assert lib.pr_token_features_workspace(1, 16896, 151936, 0) == 0
+    # Few long rows: split rows need one 32-byte partial state per workgroup.
+    ws = lib.pr_token_features_workspace(1, 4, 151936, 0)
+    assert ws > 0 and ws % (4 * 32) == 0
+    assert lib.pr_token_features_workspace(0, 0, 100, 0) == 0
+
+
+@pytest.mark.parametrize("case", ["V<2", "stride<V", "bad dtype", "null logits", "n<0", "null out",
+                                  "misaligned"])
+def test_invalid_arguments_rejected_on_host(case):
+    lib = ensure_built()
+    from paper_2608_28726_amd import _abi
+    feats = _abi.TokenFeatures(*([8] * 10))  # never dereferenced: the call must fail first
+    args = dict(logits=C.c_void_p(64), dtype=1, n=4, V=100, stride=100, ids=C.c_void_p(64),
+                temps=C.c_void_p(64), out=C.byref(feats))
+    if case == "V<2":
+        args["V"], args["stride"] = 1, 1
+    elif case == "stride<V":
+        args["stride"] = 99
+    elif case == "bad dtype":
+        args["dtype"] = 7
+    elif case == "null logits":
+        args["logits"] = None
+    elif case == "n<0":
+        args["n"] = -1
+    elif case == "null out":
+        args["out"] = None
+    elif case == "misaligned":
+        args["logits"] = C.c_void_p(65)
+    st = lib.pr_token_features(args["logits"], args["dtype"], args["n"], args["V"], args["stride"], args["ids"],
+                               args["temps"], None, args["out"], None, 0, None)
+    assert st == _abi.PR_ERR_INVALID_ARG
+
+
+def test_other_entry_points_reject_bad_arguments():
+    lib = ensure_built()
+    from paper_2608_28726_amd import _abi
+    assert lib.pr_route(None, 5, 0.5, None, None, None) == _abi.PR_ERR_INVALID_ARG
+    assert lib.pr_route(None, -1, 0.5, None, None, None) == _abi.PR_ERR_INVALID_ARG
+    agg = _abi.RequestAgg()
+    assert lib.pr_request_aggregate(None, None, 3, None, C.byref(agg), None) == _abi.PR_ERR_INVALID_ARG
+    assert lib.pr_request_aggregate(None, None, 0, None, C.byref(agg), None) == _abi.PR_OK
+    bad = _abi.AggParams()
+    lib.pr_agg_params_default(C.byref(bad))
+    bad.q = 1.5
+    feats = _abi.TokenFeatures(*([8] * 10))
+    assert lib.pr_request_aggregate(C.byref(feats), C.c_void_p(64), 3, C.byref(bad), C.byref(agg),
+                                    None) == _abi.PR_ERR_INVALID_ARG
+    h = C.c_void_p()
+    assert lib.pr_stream_create(0, 10, None, C.byref(h)) == _abi.PR_ERR_INVALID_ARG
+    assert lib.pr_stream_step(None, None, 1, 0, 100, 100, None, None, None, None, None, None) == \
+        _abi.PR_ERR_INVALID_ARG
+    assert lib.pr_stream_finish(None, None, 1, 0.5, None, None, None) == _abi.PR_ERR_INVALID_ARG
+    lib.pr_stream_destroy(None)  # ignored
+    # zero rows: valid, nothing launched
+    feats = _abi.TokenFeatures(*([8] * 10))
+    assert lib.pr_token_features(None, 0, 0, 100, 100, None, None, None, C.byref(feats), None, 0, None) == \
+        _abi.PR_OK

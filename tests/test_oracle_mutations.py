@@ -35,8 +35,9 @@ FEATURE_MUTANTS = {
     "margin unscaled": ("margin = (z[a] - z_second) / T", "margin = (z[a] - z_second)"),
     "maxprob from full softmax": ("maxprob = 1.0 / S_N", "maxprob = 1.0 / S"),
     "bf16 decode shift": ("<< np.uint32(16)", "<< np.uint32(15)"),
-    "logprob of argmax": ("logprob = u[y] - lse if e[y] > 0.0 else -math.inf",
-                          "logprob = u[a] - lse"),
+    "logprob of argmax": ("        logprob = u[y] - lse\n", "        logprob = u[a] - lse\n"),
+    "logprob underflow to -inf": ("        logprob = u[y] - lse\n",
+                                  "        logprob = u[y] - lse if e[y] > 0.0 else -math.inf\n"),
 }
 
 

@@ -43,6 +43,9 @@ def test_flags():
         assert r["flags"] == oracle.FLAG_NONFINITE and math.isnan(r["lse"]) and r["rank"] == -1
     r = oracle.token_features(np.full(4, -np.inf, dtype=np.float32), "f32", 1, 1.0)
     assert r["flags"] == oracle.FLAG_NONFINITE
+    zz = z.copy()
+    zz[0] = math.nan
+    assert oracle.token_features(zz, "f32", -1, 1.0)["flags"] == oracle.FLAG_NONFINITE | oracle.FLAG_BAD_ID
     big = np.array([2.0 ** 101, 0.0], dtype=np.float32)
     assert oracle.token_features(big, "f32", 0, 1.0)["flags"] == oracle.FLAG_BAD_TP
     assert oracle.token_features(big, "f32", 0, 2.0)["flags"] == 0
