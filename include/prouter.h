@@ -46,8 +46,9 @@ typedef enum pr_dtype { PR_F32 = 0, PR_BF16 = 1 } pr_dtype;
                                       outputs NaN, all integer outputs -1                     */
 #define PR_FLAG_BAD_ID 2u          /* sampled id outside [0, V): logprob NaN, rank -1; the
                                       other outputs are still valid                           */
-#define PR_FLAG_BAD_TP 4u          /* temperature not finite or <= 0, top-p NaN or <= 0, or
-                                      |max logit| > 2^100 * T; outputs as for NONFINITE       */
+#define PR_FLAG_BAD_TP 4u          /* temperature not finite or below 2^-100, top-p NaN or
+                                      <= 0, or |max logit| > 2^100 * T; outputs as for
+                                      NONFINITE (which is still reported when it applies)     */
 #define PR_FLAG_OUTSIDE_NUCLEUS 8u /* top-p on and the sampled token lies outside the
                                       nucleus: logprob = -inf, rank > cutoff                  */
 
@@ -130,7 +131,7 @@ size_t pr_token_features_workspace(pr_dtype dtype, int64_t n_rows, int32_t vocab
  *                r * row_stride. Requires vocab >= 2, row_stride >= vocab and
  *                the base aligned to the element size.
  *   sampled_ids  int32 [n_rows], the emitted token of each row.
- *   temperature  float [n_rows], per-row temperature (> 0).
+ *   temperature  float [n_rows], per-row temperature (finite, >= 2^-100).
  *   top_p        float [n_rows] or NULL (off). P >= 1 switches a row's
  *                truncation off; 0 < P < 1 keeps the shortest prefix of the
  *                order whose mass reaches P of the total.

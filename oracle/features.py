@@ -20,8 +20,9 @@ R1  Logits arrive as IEEE float32 or bfloat16 bit patterns; they are decoded
 R2  Token order: v precedes w iff z_v > z_w, or z_v == z_w and v < w, on the
     raw (pre-temperature) values; -0 == +0. argmax is the first token of this
     order, rank(y) is the 1-based position of y in it.
-R3  Temperature divides the logits: u = z / T. T must be finite and > 0, and
-    |z_argmax| / T must not exceed 2**100; otherwise the row is flagged.
+R3  Temperature divides the logits: u = z / T. T must be finite and at least
+    2**-100, and |z_argmax| / T must not exceed 2**100; otherwise the row is
+    flagged (the bounds keep every scaled logit inside float32's range).
 R4  Top-p keeps the shortest prefix of the order whose probability mass
     reaches P: k = min{ j : C_j >= P * S }, C_j the mass of the first j
     tokens, S the total. P >= 1 (or no P) keeps all V tokens; P <= 0 or NaN
@@ -50,6 +51,7 @@ FLAG_BAD_TP = 4  # bad temperature or top-p                           (R3, R4)
 FLAG_OUTSIDE_NUCLEUS = 8  # sampled token not inside the top-p nucleus (R4)
 
 _TEMP_RANGE = 2.0 ** 100  # R3: |z_argmax| / T may not exceed this
+_MIN_TEMPERATURE = 2.0 ** -100  # R3: smallest accepted temperature
 
 FLOAT_FEATURES = ("max_logit", "lse", "entropy", "logprob", "maxprob", "margin")
 INT_FEATURES = ("rank", "argmax", "cutoff")
@@ -100,7 +102,7 @@ def token_features(raw_row, dtype: str, y: int, T: float, P: float | None = None
     flags = FLAG_BAD_ID if bad_id else 0  # R7: a bad id is reported in every case
     if np.isnan(z).any() or np.isposinf(z).any() or np.isneginf(z).all():
         flags |= FLAG_NONFINITE
-    if not (math.isfinite(T) and T > 0.0):
+    if not (math.isfinite(T) and T >= _MIN_TEMPERATURE):
         flags |= FLAG_BAD_TP
     if P is not None and (math.isnan(P) or P <= 0.0):
         flags |= FLAG_BAD_TP

@@ -127,13 +127,26 @@ __device__ __forceinline__ void wave_top2(float& t1, int32_t& t1i, float& t2) {
 }
 
 // Rescale factor from a stretch's reference a_l to the row reference A.
-// A stretch that saw no finite logit contributes nothing (but NaN sums stay NaN).
+// A stretch that saw no finite logit contributes nothing (but NaN sums stay
+// NaN); its reference may be a sentinel while A is -inf, so no exponent is
+// formed for it.
 __device__ __forceinline__ void rebase(float m_l, float a_l, float A, float& S, float& E) {
+  if (m_l == -INFINITY) {
+    S *= 0.0f;
+    E *= 0.0f;
+    return;
+  }
   const float d = fmaxf(a_l - A, -kBig);
-  const float s = (m_l == -INFINITY) ? 0.0f : fast_exp2(d);
+  const float s = fast_exp2(d);
   E = s * E + (s * d) * S;
   S = s * S;
 }
+
+// Smallest accepted temperature: keeps log2(e) / T finite in float32.
+constexpr float kMinTemperature = 0x1p-100f;
+
+// A temperature the path accepts: finite and at least 2^-100.
+__device__ __forceinline__ bool temperature_ok(float T) { return T >= kMinTemperature && T < INFINITY; }
 
 // Sortable 32-bit key of a float: unsigned order equals numeric order,
 // -0 maps to +0, NaN sorts above +inf.

@@ -233,7 +233,9 @@ template <typename Tin>
 __device__ RowCtx row_ctx(const RowArgs& a, int64_t r, const void* row) {
   RowCtx cx;
   const float T = a.temperature[r];
-  cx.c = kLog2e / T;
+  // A rejected temperature still gets a finite scale, so that the
+  // non-finite-logit check does not depend on it.
+  cx.c = temperature_ok(T) ? kLog2e / T : kLog2e;
   cx.h = head_elems<Tin>(row, a.V);
   const int32_t y = a.sampled_ids[r];
   if (y >= 0 && y < a.V) {
@@ -311,7 +313,7 @@ __device__ void finalize_row(const RowArgs& a, int64_t r, const Partial& p, cons
                              float* conf) {
   const float T = a.temperature[r];
   uint32_t flags = 0;
-  if (!(T > 0.0f) || !(T < INFINITY)) flags |= PR_FLAG_BAD_TP;
+  if (!temperature_ok(T)) flags |= PR_FLAG_BAD_TP;
   const bool nonfinite = !(fabsf(p.S) < INFINITY) || p.m == INFINITY || p.m == -INFINITY;
   if (nonfinite) flags |= PR_FLAG_NONFINITE;
   if (!flags && fabsf(p.m) > ldexpf(T, 100)) flags |= PR_FLAG_BAD_TP;

@@ -75,8 +75,11 @@ def _special_rows(V, rng):
     rows.append((np.full(V, -np.inf), 0, 1.0))                 # all -inf
     rows.append((base.copy(), -1, 1.0))                        # bad id
     rows.append((base.copy(), V, 1.0))                         # bad id
-    for T in (0.0, -1.0, math.inf, math.nan):
+    for T in (0.0, -1.0, math.inf, math.nan, 2.0 ** -101):
         rows.append((base.copy(), 1, T))                       # bad temperature
+    r = base.copy(); r[0] = np.nan
+    rows.append((r, 1, 0.0))                                   # NaN and bad temperature
+    rows.append((np.zeros(V), 1, 2.0 ** -100))                 # smallest temperature
     r = rng.choice([-1.0, 0.0, 0.5, 1.0], size=V)
     for y in sorted({0, 1, V // 2, V - 2, V - 1}):
         rows.append((r, y, 1.0))                               # ties everywhere

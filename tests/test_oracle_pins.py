@@ -31,7 +31,7 @@ def test_flags():
     r = oracle.token_features(z, "f32", 16, 1.0)
     assert r["flags"] == oracle.FLAG_BAD_ID and r["rank"] == -1 and math.isnan(r["logprob"])
     assert r["entropy"] == pytest.approx(math.log(16))
-    for T in (0.0, -1.0, math.inf, math.nan):
+    for T in (0.0, -1.0, math.inf, math.nan, 2.0 ** -101):
         r = oracle.token_features(z, "f32", 1, T)
         assert r["flags"] == oracle.FLAG_BAD_TP and math.isnan(r["entropy"]) and r["argmax"] == -1
     for P in (0.0, -0.5, math.nan):
@@ -49,6 +49,10 @@ def test_flags():
     big = np.array([2.0 ** 101, 0.0], dtype=np.float32)
     assert oracle.token_features(big, "f32", 0, 1.0)["flags"] == oracle.FLAG_BAD_TP
     assert oracle.token_features(big, "f32", 0, 2.0)["flags"] == 0
+    assert oracle.token_features(np.zeros(4, dtype=np.float32), "f32", 0, 2.0 ** -100)["flags"] == 0
+    zz = z.copy()
+    zz[2] = math.nan
+    assert oracle.token_features(zz, "f32", 0, 0.0)["flags"] == oracle.FLAG_NONFINITE | oracle.FLAG_BAD_TP
 
 
 def test_exact_boundary_is_flagged_ambiguous():
