@@ -325,17 +325,25 @@ __device__ void finalize_row(const RowArgs& a, int64_t r, const Partial& p, cons
   float max_logit = qnan, lse = qnan, entropy = qnan, logprob = qnan, maxprob = qnan, margin = qnan;
   int32_t rank = -1, argmax = -1, cutoff = -1;
   if (!(flags & (PR_FLAG_NONFINITE | PR_FLAG_BAD_TP))) {
-    const float lnS = logf(p.S);
+    // S and E are relative to A = round(M * c). The exact residual
+    // delta = M * c - A moves them to the exact reference M * c, so that the
+    // largest logit contributes exactly 2^0 (this matters for large |M| / T).
+    const float A = p.m * cx.c;
+    const float delta = fmaf(p.m, cx.c, -A);
+    const float sc = fast_exp2(-delta);
+    const float S = p.S * sc;
+    const float E = sc * fmaf(-delta, p.S, p.E);
+    const float lnS = logf(S);
     max_logit = p.m / T;
     lse = max_logit + lnS;
-    entropy = lnS - kLn2 * (p.E / p.S);
-    maxprob = 1.0f / p.S;
+    entropy = lnS - kLn2 * (E / S);
+    maxprob = 1.0f / S;
     margin = (p.t1 - p.t2) / T;
     argmax = p.t1i;
     cutoff = a.V;
     if (cx.y >= 0) {
       rank = static_cast<int32_t>(1u + p.cnt + fix);
-      const float xy = fmaf(cx.zy, cx.c, -(p.m * cx.c));
+      const float xy = fmaf(cx.zy, cx.c, -A) - delta;
       logprob = kLn2 * xy - lnS;
     } else {
       flags |= PR_FLAG_BAD_ID;
