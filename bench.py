@@ -95,13 +95,24 @@ def cpu_baseline(torch, batch, feats_gpu, seconds):
     elapsed = time.perf_counter() - t0
     # parity spot check of the sample against the GPU's features
     bad = 0
+    detail = {}
     for k in ("max_logit", "lse", "entropy", "logprob", "maxprob", "margin"):
         g = feats_gpu[k][:n].cpu().numpy().astype(np.float64)
         o = np.array([d[k] for d in res])
         ok = (np.abs(g - o) <= 1e-5 + 1e-4 * np.abs(o)) | (np.isnan(g) & np.isnan(o)) | (g == o)
         bad += int((~ok).sum())
+        if (~ok).any():
+            i = np.flatnonzero(~ok)[:3]
+            detail[k] = {"count": int((~ok).sum()), "rows": i.tolist(), "gpu": g[i].tolist(), "oracle": o[i].tolist()}
     for k in ("rank", "argmax", "cutoff"):
-        bad += int((feats_gpu[k][:n].cpu().numpy() != np.array([d[k] for d in res])).sum())
+        g = feats_gpu[k][:n].cpu().numpy()
+        o = np.array([d[k] for d in res])
+        bad += int((g != o).sum())
+        if (g != o).any():
+            i = np.flatnonzero(g != o)[:3]
+            detail[k] = {"count": int((g != o).sum()), "rows": i.tolist(), "gpu": g[i].tolist(), "oracle": o[i].tolist()}
+    if detail:
+        log(f"[bench] parity detail: {json.dumps(detail)}")
     cores = 1
     return {
         "value": n / elapsed,

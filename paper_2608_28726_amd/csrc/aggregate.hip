@@ -3,26 +3,23 @@
 // ship iff p >= tau; Sec. 4.2, Table "ablation": a quantile summary of the
 // sequence as verifier input).
 //
-// One workgroup per request. For each confidence column
-// A = (logprob, maxprob, -entropy, margin) it computes the count, the mean
-// (double sums), the minimum and the exact nearest-rank q-quantile by a
-// four-pass byte-wise radix select over order-preserving 32-bit keys, with
-// a 256-bin histogram in LDS. The same code serves the offline ragged batch
-// (segments given by offsets) and the streaming state (each slot's history).
+// One workgroup per request, one wave per confidence column
+// A = (logprob, maxprob, -entropy, margin): count, mean (double sums),
+// minimum and the exact nearest-rank q-quantile by a four-pass byte-wise radix
+// select over order-preserving 32-bit keys (a 256-bin LDS histogram per wave
+// and a wave prefix scan per pass). The same code serves the offline ragged
+// batch (segments given by offsets) and the streaming state (each slot's
+// history).
 #include "aggregate.h"
 
 namespace pr {
 
 namespace {
 
-constexpr int kAggBlock = 256;
+// Four waves per workgroup: wave f summarises confidence column f.
+constexpr int kAggBlock = 4 * kWave;
 
-struct AggOut {
-  double mean_d;  // unrounded mean, used by the score
-  float mean, min, quant;
-};
-
-// Confidence column f of row r of the per-token feature arrays.
+// Confidence column of the per-token feature arrays (entropy is negated).
 struct FeatCol {
   const float* p;
   bool negate;
@@ -34,96 +31,87 @@ struct HistCol {
   __device__ __forceinline__ float operator()(int64_t r) const { return p[r]; }
 };
 
-// Block-wide summaries of n values get(lo + i). All threads return the result.
-template <int BLOCK, typename Get>
-__device__ AggOut block_summaries(Get get, int64_t lo, int64_t n, int64_t j, bool quant_ok) {
-  constexpr int NW = BLOCK / kWave;
-  __shared__ double sh_sum[NW];
-  __shared__ float sh_min[NW];
-  __shared__ uint32_t sh_nan[NW];
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t sh_prefix, sh_j;
-  const int t = threadIdx.x;
-  const int lane = t % kWave, w = t / kWave;
-  const float qnan = __uint_as_float(0x7fc00000u);
+__device__ __forceinline__ uint32_t wave_incl_scan_u(uint32_t v, int lane) {
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const uint32_t t = __shfl_up(v, o);
+    if (lane >= o) v += t;
+  }
+  return v;
+}
 
+// Sum (double), minimum and NaN presence of the wave's n values get(lo + k).
+template <typename Get>
+__device__ void wave_stats(Get get, int64_t lo, int64_t n, double& sum, float& mn, bool& has_nan) {
+  const int lane = threadIdx.x % kWave;
   double s = 0.0;
-  float mn = INFINITY;
-  uint32_t has_nan = 0;
-  for (int64_t i = t; i < n; i += BLOCK) {
-    const float v = get(lo + i);
+  float m = INFINITY;
+  uint32_t nan = 0;
+  for (int64_t k = lane; k < n; k += kWave) {
+    const float v = get(lo + k);
     if (v != v) {
-      has_nan = 1;
+      nan = 1;
     } else {
       s += static_cast<double>(v);
-      mn = fminf(mn, v);
+      m = fminf(m, v);
     }
   }
-  s = wave_sum_d(s);
-  mn = -wave_max(-mn);
-  has_nan = wave_sum_u(has_nan);
-  if (lane == 0) {
-    sh_sum[w] = s;
-    sh_min[w] = mn;
-    sh_nan[w] = has_nan;
-  }
-  __syncthreads();
-  double tot = 0.0;
-  float gmin = INFINITY;
-  uint32_t nan_any = 0;
-  for (int k = 0; k < NW; ++k) {
-    tot += sh_sum[k];
-    gmin = fminf(gmin, sh_min[k]);
-    nan_any |= sh_nan[k];
-  }
-  AggOut o;
-  if (n == 0 || nan_any) {
-    o.mean = o.min = o.quant = qnan;
-    o.mean_d = static_cast<double>(qnan);
-    __syncthreads();
-    return o;
-  }
-  o.mean_d = tot / static_cast<double>(n);
-  o.mean = static_cast<float>(o.mean_d);
-  o.min = gmin;
-  if (!quant_ok) {
-    o.quant = qnan;
-    __syncthreads();
-    return o;
-  }
+  sum = wave_sum_d(s);
+  mn = -wave_max(-m);
+  has_nan = wave_sum_u(nan) != 0;
+}
 
-  // Radix select of the j-th smallest key, most significant byte first.
-  uint32_t prefix = 0, mask = 0;
-  if (t == 0) sh_j = static_cast<uint32_t>(j);
+// The j-th smallest (1-based) of each wave's n values, by a byte-wise radix
+// select over order-preserving keys: per pass a 256-bin histogram of the
+// keys that match the digits chosen so far, then a wave prefix scan locates
+// the bin holding the j-th key. Every wave of the block must call this with
+// the same n (it uses block barriers). hist: [4][256], sel: [4][2] in LDS.
+template <typename Get>
+__device__ float radix_select(Get get, int64_t lo, int64_t n, int64_t j, uint32_t* hist, uint32_t* sel) {
+  const int w = threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  uint32_t* h = hist + w * 256;
+  uint32_t prefix = 0, mask = 0, need = static_cast<uint32_t>(j);
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
-    for (int b = t; b < 256; b += BLOCK) hist[b] = 0;
+    for (int b = lane; b < 256; b += kWave) h[b] = 0;
     __syncthreads();
-    for (int64_t i = t; i < n; i += BLOCK) {
-      const uint32_t k = float_key(get(lo + i));
-      if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1u);
+    for (int64_t k = lane; k < n; k += kWave) {
+      const uint32_t key = float_key(get(lo + k));
+      if ((key & mask) == prefix) atomicAdd(&h[(key >> shift) & 255u], 1u);
     }
     __syncthreads();
-    if (t == 0) {
-      uint32_t need = sh_j, b = 0;
-      for (; b < 255; ++b) {
-        if (need <= hist[b]) break;
-        need -= hist[b];
+    const uint32_t c0 = h[4 * lane], c1 = h[4 * lane + 1], c2 = h[4 * lane + 2], c3 = h[4 * lane + 3];
+    const uint32_t tot = c0 + c1 + c2 + c3;
+    const uint32_t incl = wave_incl_scan_u(tot, lane);
+    const uint32_t excl = incl - tot;
+    if (need > excl && need <= incl) {
+      uint32_t r = need - excl, q = 0;
+      if (r > c0) {
+        r -= c0;
+        q = 1;
+        if (r > c1) {
+          r -= c1;
+          q = 2;
+          if (r > c2) {
+            r -= c2;
+            q = 3;
+          }
+        }
       }
-      sh_j = need;
-      sh_prefix = prefix | (b << shift);
+      sel[2 * w] = 4u * lane + q;
+      sel[2 * w + 1] = r;
     }
     __syncthreads();
-    prefix = sh_prefix;
+    prefix |= sel[2 * w] << shift;
+    need = sel[2 * w + 1];
     mask |= 255u << shift;
-    __syncthreads();
   }
-  o.quant = key_float(prefix);
-  return o;
+  return key_float(prefix);
 }
 
 __device__ int64_t quant_rank(double q, int64_t n) {
-  double qn = q * static_cast<double>(n);
+  const double qn = q * static_cast<double>(n);
   int64_t j = static_cast<int64_t>(ceil(qn));
   if (j < 1) j = 1;
   if (j > n) j = n;
@@ -154,30 +142,63 @@ __device__ void write_request(const pr_request_agg_t& out, int64_t i, int64_t n,
   if (out.score) out.score[i] = score;
 }
 
+struct AggShared {
+  uint32_t hist[4 * 256];
+  uint32_t sel[8];
+  double mean_d[4];
+  float mn[4], qu[4];
+  uint32_t nan[4];
+};
+
+// Thread 0: applies the NaN / empty rules and writes one request.
+__device__ void finish_request(const AggShared& sh, const AggParamsDev& hp, const pr_request_agg_t& out, int64_t i,
+                               int64_t n, float* score_out) {
+  const float qnan = __uint_as_float(0x7fc00000u);
+  float mean[4], mn[4], qu[4];
+  double mean_d[4];
+  for (int f = 0; f < 4; ++f) {
+    const bool bad = n == 0 || sh.nan[f];
+    mean_d[f] = bad ? static_cast<double>(qnan) : sh.mean_d[f];
+    mean[f] = bad ? qnan : static_cast<float>(sh.mean_d[f]);
+    mn[f] = bad ? qnan : sh.mn[f];
+    qu[f] = bad ? qnan : sh.qu[f];
+  }
+  const float score = head_score(hp, mean_d, mn, qu, n);
+  write_request(out, i, n, mean, mn, qu, score);
+  *score_out = score;
+}
+
 }  // namespace
 
 __global__ __launch_bounds__(kAggBlock) void aggregate_kernel(pr_token_features_t feats, const int32_t* offsets,
                                                               int32_t n_req, AggParamsDev hp,
                                                               pr_request_agg_t out) {
+  __shared__ AggShared sh;
   const int64_t i = blockIdx.x;
   if (i >= n_req) return;
   const int64_t lo = offsets[i];
   const int64_t hi = offsets[i + 1];
   const int64_t n = hi > lo ? hi - lo : 0;
-  const int64_t j = n > 0 ? quant_rank(hp.q, n) : 1;
+  const int w = threadIdx.x / kWave;
   const float* cols[4] = {feats.logprob, feats.maxprob, feats.entropy, feats.margin};
-  float mean[4], mn[4], qu[4];
-  double mean_d[4];
-  for (int f = 0; f < 4; ++f) {
-    const FeatCol get{cols[f], f == 2};
-    const AggOut o = block_summaries<kAggBlock>(get, lo, n, j, true);
-    mean[f] = o.mean;
-    mn[f] = o.min;
-    qu[f] = o.quant;
-    mean_d[f] = o.mean_d;
-    __syncthreads();
+  const FeatCol get{cols[w], w == 2};
+  double sum;
+  float mn;
+  bool nan;
+  wave_stats(get, lo, n, sum, mn, nan);
+  float q = 0.0f;
+  if (n > 0) q = radix_select(get, lo, n, quant_rank(hp.q, n), sh.hist, sh.sel);
+  if (threadIdx.x % kWave == 0) {
+    sh.mean_d[w] = n > 0 ? sum / static_cast<double>(n) : 0.0;
+    sh.mn[w] = mn;
+    sh.qu[w] = q;
+    sh.nan[w] = nan ? 1u : 0u;
   }
-  if (threadIdx.x == 0) write_request(out, i, n, mean, mn, qu, head_score(hp, mean_d, mn, qu, n));
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float score;
+    finish_request(sh, hp, out, i, n, &score);
+  }
 }
 
 __global__ __launch_bounds__(1024) void route_kernel(const float* scores, int32_t n_req, float thr, uint8_t* ship,
@@ -213,44 +234,35 @@ __global__ void stream_clear_kernel(StreamDev s, const int32_t* slots, int32_t n
   }
 }
 
-// One workgroup per finishing slot: summaries as in aggregate_kernel, with
-// the running sums and minima taken from the slot state and the quantile
-// selected from the slot's history; then the slot is cleared.
+// One workgroup per finishing slot: the running sums and minima come from the
+// slot state, the quantile is selected from the slot's history (wave f: column
+// f); then the slot is cleared.
 __global__ __launch_bounds__(kAggBlock) void stream_finish_kernel(StreamDev s, const int32_t* slots, int32_t n,
                                                                   AggParamsDev hp, float thr,
                                                                   pr_request_agg_t out, uint8_t* ship) {
+  __shared__ AggShared sh;
   const int64_t i = blockIdx.x;
   if (i >= n) return;
   const int32_t slot = slots[i];
   const bool ok = slot >= 0 && slot < s.max_slots;
   const int64_t cnt = ok ? s.count[slot] : 0;
-  const float qnan = __uint_as_float(0x7fc00000u);
-  float mean[4], mn[4], qu[4];
-  double mean_d[4];
-  const int64_t j = cnt > 0 ? quant_rank(hp.q, cnt) : 1;
   const bool kept = cnt <= s.max_len;
-  for (int f = 0; f < 4; ++f) {
-    const bool bad = cnt == 0 || (ok && ((s.nanbits[slot] >> f) & 1u));
-    if (bad) {
-      mean[f] = mn[f] = qu[f] = qnan;
-      mean_d[f] = static_cast<double>(qnan);
-      continue;
-    }
-    mean_d[f] = s.sum[slot * 4 + f] / static_cast<double>(cnt);
-    mean[f] = static_cast<float>(mean_d[f]);
-    mn[f] = s.minv[slot * 4 + f];
-    if (kept) {
-      const HistCol get{s.hist + (static_cast<int64_t>(slot) * 4 + f) * s.max_len};
-      qu[f] = block_summaries<kAggBlock>(get, 0, cnt, j, true).quant;
-    } else {
-      qu[f] = qnan;
-    }
-    __syncthreads();
+  const int w = threadIdx.x / kWave;
+  float q = __uint_as_float(0x7fc00000u);
+  if (cnt > 0 && kept) {
+    const HistCol get{s.hist + (static_cast<int64_t>(slot) * 4 + w) * s.max_len};
+    q = radix_select(get, 0, cnt, quant_rank(hp.q, cnt), sh.hist, sh.sel);
+  }
+  if (threadIdx.x % kWave == 0) {
+    sh.mean_d[w] = cnt > 0 ? s.sum[slot * 4 + w] / static_cast<double>(cnt) : 0.0;
+    sh.mn[w] = cnt > 0 ? s.minv[slot * 4 + w] : 0.0f;
+    sh.qu[w] = q;
+    sh.nan[w] = (cnt > 0 && ((s.nanbits[slot] >> w) & 1u)) ? 1u : 0u;
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    const float score = head_score(hp, mean_d, mn, qu, cnt);
-    write_request(out, i, cnt, mean, mn, qu, score);
+    float score;
+    finish_request(sh, hp, out, i, cnt, &score);
     if (ship) ship[i] = score >= thr ? 1 : 0;
     if (ok) {
       s.count[slot] = 0;

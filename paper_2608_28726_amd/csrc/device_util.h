@@ -130,8 +130,8 @@ __device__ __forceinline__ void wave_top2(float& t1, int32_t& t1i, float& t2) {
 // A stretch that saw no finite logit contributes nothing (but NaN sums stay
 // NaN); its reference may be a sentinel while A is -inf, so no exponent is
 // formed for it.
-__device__ __forceinline__ void rebase(float m_l, float a_l, float A, float& S, float& E) {
-  if (m_l == -INFINITY) {
+__device__ __forceinline__ void rebase(bool no_finite, float a_l, float A, float& S, float& E) {
+  if (no_finite) {
     S *= 0.0f;
     E *= 0.0f;
     return;

@@ -20,13 +20,14 @@ namespace pr {
 namespace {
 
 struct Lane {
-  float a;         // reference of S and E: running max * c, or kNegSentinel
+  float mw;        // running max of the wave's logits (wave-uniform in the vector loop)
+  float a;         // reference of S and E: mw * c, or kNegSentinel
   float S0, S1;    // two accumulators of sum 2^x (alternating elements)
   float E0, E1;    // two accumulators of sum 2^x * x
-  float t1, t2;    // largest and second value (t1 is also the running max)
+  float t1, t2;    // largest and second value this lane recorded
   int32_t t1i;     // index of t1 (lowest among ties)
-  uint32_t cnt_w;  // ballot counts of whole waves, each added to one lane
-  uint32_t cnt_s;  // count from this lane's scalar-path elements
+  uint32_t cnt;    // rank counts (ballot totals are added in lane 0 only)
+  float thr2;      // wave-uniform: max over the wave's lanes of t2
 };
 
 struct RowCtx {
@@ -39,17 +40,19 @@ struct RowCtx {
 };
 
 __device__ __forceinline__ void lane_init(Lane& L) {
+  L.mw = -INFINITY;
   L.a = kNegSentinel;
   L.S0 = L.S1 = L.E0 = L.E1 = 0.0f;
   L.t1 = -INFINITY;
   L.t2 = -INFINITY;
   L.t1i = kNoIndex;
-  L.cnt_w = 0;
-  L.cnt_s = 0;
+  L.cnt = 0;
+  L.thr2 = -INFINITY;
 }
 
-// Moves the lane's reference to the new running max m_new (> t1).
+// Moves the lane's reference up to a_new = m_new * c (m_new >= the old max).
 __device__ __forceinline__ void lane_rescale(Lane& L, float m_new, float c) {
+  L.mw = m_new;
   const float a_new = m_new * c;
   const float d = fmaxf(L.a - a_new, -kBig);
   const float s = fast_exp2(d);
@@ -61,7 +64,9 @@ __device__ __forceinline__ void lane_rescale(Lane& L, float m_new, float c) {
   L.a = a_new;
 }
 
-// NV vectors of one lane; vector u has vector index i + u * BLOCK.
+// NV vectors of one lane; vector u has vector index i + u * BLOCK. Every lane
+// of the wave calls this together (wave-uniform control flow), so the
+// cross-lane steps below see all 64 lanes.
 template <typename Tin, int NV, int BLOCK>
 __device__ __forceinline__ void consume(const uint4 (&v)[NV], int64_t i, const RowCtx& cx, Lane& L) {
   constexpr int VEC = Elem<Tin>::kVec;
@@ -73,30 +78,37 @@ __device__ __forceinline__ void consume(const uint4 (&v)[NV], int64_t i, const R
 #pragma unroll
   for (int k = 1; k < NV * VEC; ++k) cmax = fmaxf(cmax, z[k]);
 
-  // Top-1/top-2 and the running max change rarely once the row is under way.
-  if (cmax > L.t2) {
-    if (cmax > L.t1) lane_rescale(L, cmax, cx.c);
+  // The wave shares one reference, its running maximum: every exponent
+  // argument stays <= 0 and the reference moves only on a new wave maximum.
+  if (__any(cmax > L.mw)) lane_rescale(L, wave_max(cmax), cx.c);
+
+  // Top-1/top-2. An element no larger than thr2 cannot change the row's
+  // result: some lane already holds two values >= it at lower indices (every
+  // chunk lies above the previous ones in index order). thr2 rises quickly,
+  // so the per-element update below runs on few chunks.
+  if (__any(cmax > L.thr2)) {
+    if (cmax > L.t2) {
 #pragma unroll
-    for (int u = 0; u < NV; ++u) {
+      for (int u = 0; u < NV; ++u) {
 #pragma unroll
-      for (int k = 0; k < VEC; ++k) {
-        const float zk = z[u * VEC + k];
-        if (zk > L.t1) {
-          L.t2 = L.t1;
-          L.t1 = zk;
-          L.t1i = static_cast<int32_t>(cx.h + (i + u * BLOCK) * VEC + k);
-        } else if (zk > L.t2) {
-          L.t2 = zk;
+        for (int k = 0; k < VEC; ++k) {
+          const float zk = z[u * VEC + k];
+          if (zk > L.t1) {
+            L.t2 = L.t1;
+            L.t1 = zk;
+            L.t1i = static_cast<int32_t>(cx.h + (i + u * BLOCK) * VEC + k);
+          } else if (zk > L.t2) {
+            L.t2 = zk;
+          }
         }
       }
     }
+    L.thr2 = wave_max(L.t2);
   }
 
   // Rank of y: a vector wholly before y counts z >= z_y (z > next_below(z_y)),
   // any other vector counts z > z_y; ties before y inside y's own vector are
-  // added once when the row is finalised.
-  // The ballot totals are wave-wide: they go to the first active lane only,
-  // since lanes of one wave may run different loops over a stretch.
+  // added once when the row is finalised. Ballot totals are wave-wide.
   if (__any(cmax > cx.thr_lo)) {
     uint32_t c = 0;
 #pragma unroll
@@ -106,10 +118,11 @@ __device__ __forceinline__ void consume(const uint4 (&v)[NV], int64_t i, const R
 #pragma unroll
       for (int k = 0; k < VEC; ++k) c += __popcll(__ballot(z[u * VEC + k] > thr));
     }
-    const int first = __ffsll(static_cast<unsigned long long>(__ballot(1))) - 1;
-    if (static_cast<int>(__lane_id()) == first) L.cnt_w += c;
+    if (__lane_id() == 0) L.cnt += c;
   }
 
+  // Sum of 2^x and of 2^x * x. A masked logit (-inf) has x = -inf and
+  // 2^x = 0; x is clamped to a finite value so that 0 * x stays 0.
   const float na = -L.a;
 #pragma unroll
   for (int k = 0; k < NV * VEC; k += 2) {
@@ -124,17 +137,17 @@ __device__ __forceinline__ void consume(const uint4 (&v)[NV], int64_t i, const R
   }
 }
 
-// One element outside the aligned vectors (row head or tail).
+// One element outside the aligned vectors (row head or tail), per lane.
 __device__ __forceinline__ void consume_scalar(float z, int64_t idx, const RowCtx& cx, Lane& L) {
+  if (z > L.mw) lane_rescale(L, z, cx.c);
   if (z > L.t1) {
-    lane_rescale(L, z, cx.c);
     L.t2 = L.t1;
     L.t1 = z;
     L.t1i = static_cast<int32_t>(idx);
   } else if (z > L.t2) {
     L.t2 = z;
   }
-  if (cx.y >= 0) L.cnt_s += (z > cx.zy || (z == cx.zy && idx < cx.y)) ? 1u : 0u;
+  if (cx.y >= 0) L.cnt += (z > cx.zy || (z == cx.zy && idx < cx.y)) ? 1u : 0u;
   const float x = fmaf(z, cx.c, -L.a);
   const float e = fast_exp2(x);
   L.S0 += e;
@@ -152,7 +165,7 @@ __device__ Partial block_merge(Lane& L, float c) {
   const int w = threadIdx.x / kWave;
 
   const float mw = wave_max(L.t1);
-  const uint32_t cw = wave_sum_u(L.cnt_w + L.cnt_s);
+  const uint32_t cw = wave_sum_u(L.cnt);
   float t1 = L.t1, t2 = L.t2;
   int32_t t1i = L.t1i;
   wave_top2(t1, t1i, t2);
@@ -169,7 +182,7 @@ __device__ Partial block_merge(Lane& L, float c) {
   for (int k = 1; k < NW; ++k) M = fmaxf(M, sh_m[k]);
   const float A = M * c;
   float S = L.S0 + L.S1, E = L.E0 + L.E1;
-  rebase(L.t1, L.a, A, S, E);
+  rebase(L.a == kNegSentinel, L.a, A, S, E);
   S = wave_sum(S);
   E = wave_sum(E);
   if (lane == 0) {
@@ -213,7 +226,7 @@ __device__ Partial merge_partials(const Partial* parts, int G, float c) {
   p.pad = 0;
   for (int g = 0; g < G; ++g) {
     Partial q = parts[g];
-    rebase(q.m, q.m * c, A, q.S, q.E);
+    rebase(q.m == -INFINITY, q.m * c, A, q.S, q.E);
     p.S += q.S;
     p.E += q.E;
     top2_merge(p.t1, p.t1i, p.t2, q.t1, q.t1i, q.t2);
@@ -252,8 +265,31 @@ __device__ RowCtx row_ctx(const RowArgs& a, int64_t r, const void* row) {
   return cx;
 }
 
+// Logits are read exactly once: nontemporal loads do not keep them cached.
+__device__ __forceinline__ uint4 load_stream(const uint4* p) {
+#ifndef PR_CACHED_LOADS
+  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+#else
+  return *p;
+#endif
+}
+
 // Scan of the vector index range [vb, ve) of one row by one workgroup,
 // plus the scalar head (first) / tail (last) elements.
+// All-(-inf) vector: padding for lanes past the end of a stretch.
+template <typename Tin>
+__device__ __forceinline__ uint4 neg_inf_vec() {
+  const uint32_t w = sizeof(Tin) == 2 ? 0xff80ff80u : 0xff800000u;
+  return make_uint4(w, w, w, w);
+}
+
+// Scan of the vector index range [vb, ve) of one row by one workgroup,
+// plus the scalar head (first) / tail (last) elements. Loop trip counts are
+// uniform across each wave: full steps while the wave's last lane still has
+// U vectors, then single-vector steps in which lanes past the end see -inf
+// (a token of probability 0 that changes no result).
 template <typename Tin, int BLOCK, int U>
 __device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve, bool do_head, bool do_tail,
                              int64_t nvec, const RowCtx& cx, Lane& L) {
@@ -261,17 +297,23 @@ __device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve,
   const Tin* base = static_cast<const Tin*>(row) + cx.h;
   const uint4* vp = reinterpret_cast<const uint4*>(base);
   const int t = threadIdx.x;
-  if (do_head && t < cx.h) consume_scalar(Elem<Tin>::load1(row, t), t, cx, L);
+  const int wave_first = t - static_cast<int>(__lane_id());
+  if (do_head) {
+    if (t < cx.h) consume_scalar(Elem<Tin>::load1(row, t), t, cx, L);
+    const float m = wave_max(L.mw);  // one reference for the whole wave again
+    if (m > L.mw) lane_rescale(L, m, cx.c);
+  }
   int64_t i = vb + t;
-  for (; i + (U - 1) * BLOCK < ve; i += U * BLOCK) {
+  int64_t i_last = vb + wave_first + (kWave - 1);  // the wave's last lane
+  for (; i_last + (U - 1) * BLOCK < ve; i += U * BLOCK, i_last += U * BLOCK) {
     uint4 v[U];
 #pragma unroll
-    for (int u = 0; u < U; ++u) v[u] = vp[i + u * BLOCK];
+    for (int u = 0; u < U; ++u) v[u] = load_stream(vp + i + u * BLOCK);
     consume<Tin, U, BLOCK>(v, i, cx, L);
   }
-  for (; i < ve; i += BLOCK) {
+  for (int64_t i_first = i - __lane_id(); i_first < ve; i += BLOCK, i_first += BLOCK) {
     uint4 v[1];
-    v[0] = vp[i];
+    v[0] = i < ve ? load_stream(vp + i) : neg_inf_vec<Tin>();
     consume<Tin, 1, BLOCK>(v, i, cx, L);
   }
   if (do_tail) {
@@ -394,8 +436,14 @@ __device__ void stream_update(const StreamDev& s, int32_t slot, const float* con
 // MODE 1: G workgroups per row write partial states to a.ws.
 // MODE 2: streaming; G workgroups per row, the last to finish merges,
 //         finalises and updates the request slot.
+// Occupancy target: 8 waves per SIMD keep enough loads in flight.
+#ifndef PR_ROW_WAVES_PER_EU
+#define PR_ROW_WAVES_PER_EU 8
+#endif
+
 template <typename Tin, int BLOCK, int U, int MODE>
-__global__ __launch_bounds__(BLOCK) void row_features_kernel(RowArgs a) {
+__global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(PR_ROW_WAVES_PER_EU)))
+void row_features_kernel(RowArgs a) {
   const int G = a.G;
   const int64_t r = blockIdx.x / G;
   const int g = blockIdx.x % G;
@@ -462,13 +510,24 @@ __global__ __launch_bounds__(BLOCK) void row_merge_kernel(RowArgs a) {
 
 namespace {
 
-constexpr int kBlock = 256;
+#ifndef PR_ROW_BLOCK
+#define PR_ROW_BLOCK 128
+#endif
+#ifndef PR_UNROLL_BF16
+#define PR_UNROLL_BF16 2
+#endif
+#ifndef PR_UNROLL_F32
+#define PR_UNROLL_F32 4
+#endif
+
+constexpr int kBlock = PR_ROW_BLOCK;
 constexpr int kTargetBlocks = 2048;  // 8 workgroups per CU on 256 CUs
 constexpr int kMaxSplit = 64;
 
+// 16-byte vectors per lane per loop step.
 template <typename Tin>
 constexpr int unroll_for() {
-  return Elem<Tin>::kVec == 8 ? 4 : 8;  // 32 logits per lane per step
+  return Elem<Tin>::kVec == 8 ? PR_UNROLL_BF16 : PR_UNROLL_F32;
 }
 
 }  // namespace
