@@ -1,0 +1,108 @@
+"""Top-p (nucleus) features: exact cutoff index, rank and renormalised
+features, HIP path vs the fp64 oracle."""
+
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_28726_amd as pr
+from paper_2608_28726_amd import workloads as wl
+from tests.gpu_common import compare_features, gpu_features, oracle_features, require_gpu, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    require_gpu()
+
+
+def _run(z, ids, T, P, dtype=torch.float32):
+    logits, ids, T, P = to_dev(torch.as_tensor(z, dtype=torch.float32).to(dtype), torch.as_tensor(ids, dtype=torch.int32),
+                               torch.as_tensor(T, dtype=torch.float32), torch.as_tensor(P, dtype=torch.float32))
+    return logits, ids, T, P
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("V", [2, 7, 8, 64, 1000, 32000])
+def test_topp_random_rows(V, dtype):
+    rng = np.random.default_rng(100 + V)
+    n = 24
+    z = rng.normal(0, rng.uniform(0.5, 4, (n, 1)), (n, V))
+    z[np.arange(n), rng.integers(0, V, n)] += rng.uniform(0, 15, n)
+    T = rng.uniform(0.3, 1.2, n)
+    P = rng.uniform(0.05, 0.99, n)
+    P[:4] = [1.0, 2.0, 1e-7, 0.999]
+    ids = rng.integers(0, V, n)
+    logits, ids, T, P = _run(z, ids, T, P, dtype)
+    print(f"case topp random V={V} {dtype}", flush=True)
+    compare_features(gpu_features(logits, ids, T, P), oracle_features(logits, ids, T, P))
+
+
+def test_topp_special_rows():
+    V = 64
+    rows, ids, Ts, Ps = [], [], [], []
+    def add(z, y, T, P):
+        rows.append(np.asarray(z, dtype=np.float64)); ids.append(y); Ts.append(T); Ps.append(P)
+    add(np.zeros(V), 3, 1.0, 0.5)            # uniform: k = 32
+    add(np.zeros(V), 40, 1.0, 0.5)           # sampled token outside the nucleus
+    add(np.zeros(V), 0, 1.0, 0.3)            # k = ceil(0.3 * 64) = 20
+    z = np.full(V, -np.inf); z[5] = 1.0
+    add(z, 5, 1.0, 0.9)                      # one-hot via -inf
+    add(z, 6, 1.0, 0.9)                      # masked sampled token
+    add(np.arange(V) * -0.5, 2, 0.7, 0.8)    # geometric
+    add(np.zeros(V), 1, 1.0, 0.0)            # P = 0: flagged
+    add(np.zeros(V), 1, 1.0, math.nan)       # P = NaN: flagged
+    add(np.zeros(V), 1, 1.0, -0.5)           # P < 0: flagged
+    add(np.where(np.arange(V) < 10, 2.0, 0.0), 9, 1.0, 0.5)   # tie block at the top
+    logits, ids, T, P = _run(np.stack(rows), ids, Ts, Ps)
+    compare_features(gpu_features(logits, ids, T, P), oracle_features(logits, ids, T, P))
+
+
+@pytest.mark.parametrize("V", [262144, 151936])
+def test_topp_massive_ties_radix_path(V):
+    """Rows whose boundary bins hold more logits than the LDS sort takes:
+    all-equal bf16 rows and rows with a few distinct values."""
+    rng = np.random.default_rng(V)
+    rows = [np.zeros(V), rng.choice([0.0, 0.5, 1.0], size=V), np.full(V, 3.0)]
+    rows[2][: V // 3] = 3.5
+    ids = [7, int(rng.integers(0, V)), V - 1]
+    logits, ids, T, P = _run(np.stack(rows), ids, [1.0, 0.9, 1.1], [0.37, 0.8, 0.6], torch.bfloat16)
+    print(f"case topp ties V={V}", flush=True)
+    compare_features(gpu_features(logits, ids, T, P), oracle_features(logits, ids, T, P))
+
+
+def test_topp_workload_scaled():
+    """The top-p row model (V = 262,144 float32, T ~ U[0.3,1.2], P ~ U[0.8,0.95]) on a few requests."""
+    w = wl.scaled(wl.WORKLOADS["topp_128x256_v262144_f32"], n_req=4, len_hi=6, len_lo=6)
+    b = wl.make_batch(w, device="cpu")
+    logits, ids, T, P = to_dev(b.logits, b.sampled_ids, b.temperature, b.top_p)
+    print(f"case topp workload rows={b.n_rows}", flush=True)
+    g = gpu_features(logits, ids, T, P)
+    o = oracle_features(logits, ids, T, P)
+    compare_features(g, o)
+    assert (o["flags"] & pr.FLAG_OUTSIDE_NUCLEUS == 0).all()  # the sampler stays inside the nucleus
+
+
+def test_topp_full_size():
+    """128 requests x 256 tokens of V = 262,144 float32 (34 GB) with top-p: every
+    row checked for invariants, sampled rows against the oracle."""
+    w = wl.WORKLOADS["topp_128x256_v262144_f32"]
+    b = wl.make_batch(w, device="cuda")
+    print(f"case topp full rows={b.n_rows}", flush=True)
+    feats = pr.token_features(b.logits, b.sampled_ids, b.temperature, b.top_p)
+    torch.cuda.synchronize()
+    f = {k: v.cpu().numpy() for k, v in feats.items()}
+    assert (f["flags"] & ~pr.FLAG_OUTSIDE_NUCLEUS == 0).all()
+    assert (f["cutoff"] >= 1).all() and (f["cutoff"] <= w.V).all()
+    inside = f["rank"] <= f["cutoff"]
+    assert inside.mean() > 0.999, inside.mean()
+    assert (f["maxprob"] > 0).all() and (f["maxprob"] <= 1 + 1e-6).all()
+    assert (f["entropy"] <= np.log(f["cutoff"]) + 1e-4).all() and (f["entropy"] >= -1e-5).all()
+    rng = np.random.default_rng(5)
+    rows = rng.choice(b.n_rows, 20, replace=False)
+    sel = torch.as_tensor(rows, device="cuda")
+    o = oracle_features(b.logits[sel], b.sampled_ids[sel], b.temperature[sel], b.top_p[sel])
+    compare_features(f, o, rows=rows)
