@@ -127,6 +127,123 @@ def cpu_baseline(torch, batch, feats_gpu, seconds):
     }
 
 
+def run_offline(args, torch, pr, wl, w):
+    """Offline ragged batches (features -> summaries -> route per step). Workloads
+    larger than one batch are generated as device-resident chunks of whole
+    requests; small ones are replicated so that a step never re-reads the
+    256 MB last-level cache."""
+    n_chunks = 16 if w.n_req * w.len_hi * w.V * w.elem_bytes > 40e9 else 1
+    per = w.n_req // n_chunks
+    batches = [wl.make_batch(wl.scaled(w, n_req=per, seed=w.seed + c) if n_chunks > 1 else w, device="cuda")
+               for c in range(n_chunks)]
+    copies = 1
+    one = batches[0].n_rows * w.V * w.elem_bytes
+    if n_chunks == 1 and one < 512e6:
+        copies = int(np.ceil(600e6 / one))
+        base = batches[0]
+        batches = [base] + [wl.Batch(base.workload, base.offsets, base.logits.clone(), base.sampled_ids,
+                                     base.temperature, base.top_p) for _ in range(copies - 1)]
+    torch.cuda.synchronize()
+    n_rows = sum(b.n_rows for b in batches) // copies
+    log(f"[bench] {w.name}: {n_rows} rows in {n_chunks} chunk(s), {copies} rotating copies, "
+        f"{n_rows * w.V * w.elem_bytes / 1e9:.2f} GB per step")
+    offs = [torch.as_tensor(b.offsets).cuda() for b in batches]
+    feats = [pr.token_features(b.logits, b.sampled_ids, b.temperature, b.top_p) for b in batches]
+    wss = []
+    for b in batches:
+        nb = pr.token_features_workspace(b.logits, b.top_p is not None)
+        wss.append(torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda"))
+    state = {"k": 0}
+
+    def step(ev=None):
+        group = [state["k"] % copies] if copies > 1 else range(n_chunks)
+        state["k"] += 1
+        out = None
+        for c in group:
+            b = batches[c]
+            if ev is not None and c == group[0]:
+                ev[0].record()
+            pr.token_features(b.logits, b.sampled_ids, b.temperature, b.top_p, out=feats[c], workspace=wss[c])
+            if ev is not None and c == group[-1]:
+                ev[1].record()
+            agg = pr.request_aggregate(feats[c], offs[c], q=w.q)
+            out = pr.route(agg["score"], w.tau)
+        return out
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    log(f"[bench] timing {args.steps} steps")
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        ship, n_ship = step(events[k])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kern_ms = float(np.mean([a.elapsed_time(b) for a, b in events]))
+    bytes_launch = n_rows * algorithmic_bytes_per_row(w.V, w.elem_bytes)
+    kernel = "topp_kernel" if w.P_lo is not None else "row_features_kernel"
+    if n_chunks > 1:  # events bracket all chunks' row kernels and their summaries
+        kernel += f" x{n_chunks} chunks (+summaries)"
+    extra = {"kernel": kernel, "kernel_ms": kern_ms, "bytes_per_launch": bytes_launch}
+    return batches[0], feats[0], n_rows, elapsed, kern_ms, bytes_launch, extra
+
+
+def run_stream(args, torch, pr, wl, w):
+    """Streaming decode: one pr_stream_step per decode step over the active
+    slots, pr_stream_finish for the slots whose request ends; the full
+    schedule of 1,024 steps is one timed pass."""
+    fin = wl.stream_schedule(w)
+    n_steps = int(fin.max())
+    pool = []
+    for p in range(6):  # 6 x 78 MB of distinct step inputs, cycled (above the 256 MB cache)
+        pool.append(wl.stream_step_inputs(w, 10_000 + p, np.arange(w.n_req), device="cuda"))
+    torch.cuda.synchronize()
+    st = pr.StreamState(w.n_req, n_steps, q=w.q)
+    slots_all = torch.arange(w.n_req, dtype=torch.int32, device="cuda")
+    actives = [torch.as_tensor(np.flatnonzero(fin >= s).astype(np.int32), device="cuda") for s in range(1, n_steps + 1)]
+    endings = [torch.as_tensor(np.flatnonzero(fin == s).astype(np.int32), device="cuda") for s in range(1, n_steps + 1)]
+
+    def one_pass(events=None):
+        total = 0
+        for s in range(n_steps):
+            act = actives[s]
+            n = act.shape[0]
+            logits, ids, T = pool[s % len(pool)]
+            if events is not None:
+                events[s][0].record()
+            st.step(logits[:n], act, ids[:n], T[:n])
+            if events is not None:
+                events[s][1].record()
+            if endings[s].shape[0]:
+                st.finish(endings[s], w.tau)
+            total += n
+        return total
+
+    one_pass()  # warm-up pass (also clears every slot at its finish)
+    torch.cuda.synchronize()
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_steps)]
+    t0 = time.perf_counter()
+    rows = one_pass(events)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ks = np.array([a.elapsed_time(b) for a, b in events])
+    full = np.array([a.shape[0] == w.n_req for a in actives])
+    kern_full = float(np.mean(ks[full]))
+    bytes_step = w.n_req * algorithmic_bytes_per_row(w.V, w.elem_bytes)
+    st.close()
+    extra = {"kernel": "row_features_kernel (streaming step)", "kernel_ms": kern_full,
+             "bytes_per_launch": bytes_step,
+             "step_kernel_us_p50": float(np.percentile(ks, 50) * 1e3),
+             "step_kernel_us_p99": float(np.percentile(ks, 99) * 1e3),
+             "full_steps": int(full.sum()), "steps_total": n_steps,
+             "wall_us_per_step": elapsed * 1e6 / n_steps}
+    log(f"[bench] stream: {n_steps} steps, {rows} rows, full-step kernel {kern_full * 1e3:.1f} us "
+        f"(p50 {extra['step_kernel_us_p50']:.1f} us, p99 {extra['step_kernel_us_p99']:.1f} us), "
+        f"wall {extra['wall_us_per_step']:.1f} us/step")
+    return None, None, rows, elapsed, kern_full, bytes_step, extra
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -141,45 +258,14 @@ def main():
 
     w = wl.WORKLOADS[args.workload]
     log(f"[bench] generating {w.name} on the GPU")
-    batch = wl.make_batch(w, device="cuda")
-    n_rows = batch.n_rows
-    offsets = torch.as_tensor(batch.offsets).cuda()
-    torch.cuda.synchronize()
-    log(f"[bench] rows={n_rows} V={w.V} dtype={w.dtype} bytes={n_rows * w.V * w.elem_bytes / 1e9:.2f} GB")
-
-    feats = pr.token_features(batch.logits, batch.sampled_ids, batch.temperature, batch.top_p)
-    ws_bytes = pr.token_features_workspace(batch.logits, batch.top_p is not None)
-    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device="cuda")
-
-    def step(ev=None):
-        if ev is not None:
-            ev[0].record()
-        pr.token_features(batch.logits, batch.sampled_ids, batch.temperature, batch.top_p, out=feats, workspace=ws)
-        if ev is not None:
-            ev[1].record()
-        agg = pr.request_aggregate(feats, offsets, q=w.q)
-        return pr.route(agg["score"], w.tau)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(args.steps)]
-    log(f"[bench] timing {args.steps} steps")
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for k in range(args.steps):
-        ship, n_ship = step(events[k])
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    kern_ms = [a.elapsed_time(b) for a, b in events]
-    avg_ms = float(np.mean(kern_ms))
-    ms_per_step = elapsed * 1e3 / args.steps
-    rows_per_s = n_rows * args.steps / elapsed
-    bytes_launch = n_rows * algorithmic_bytes_per_row(w.V, w.elem_bytes)
+    stream_mode = w.name.startswith("stream_")
+    runner = run_stream if stream_mode else run_offline
+    batch, feats, n_rows, elapsed, avg_ms, bytes_launch, extra = runner(args, torch, pr, wl, w)
+    steps = 1 if stream_mode else args.steps
+    ms_per_step = elapsed * 1e3 / (int(extra.get("steps_total", 0)) if stream_mode else args.steps)
+    rows_per_s = n_rows * (1 if stream_mode else args.steps) / elapsed
     achieved = bytes_launch / (avg_ms * 1e-3) / 1e9
-    log(f"[bench] {ms_per_step:.3f} ms/step, row kernel {avg_ms:.3f} ms ({achieved:.0f} GB/s), "
-        f"n_ship={int(n_ship.item())}/{w.n_req}")
+    log(f"[bench] {ms_per_step:.3f} ms/step, row kernel {avg_ms:.3f} ms ({achieved:.0f} GB/s)")
 
     traffic = None
     if os.path.exists(args.traffic_json):
@@ -195,7 +281,7 @@ def main():
         "value": rows_per_s,
         "unit": "rows/s",
         "n_gpus": 1,
-        "steps": args.steps,
+        "steps": steps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
         "higher_is_better": True,
@@ -204,17 +290,17 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "n_req": w.n_req, "rows": n_rows, "V": w.V, "logits": w.dtype,
+                   "mode": "streaming decode, one step per token" if stream_mode else "offline ragged batch",
                    "temperature": [w.T_lo, w.T_hi], "top_p": None if w.P_lo is None else [w.P_lo, w.P_hi],
                    "aggregation": f"mean/min/q={w.q} nearest-rank", "threshold": w.tau},
         "gb_per_s": achieved,
         "pct_of_hbm_peak": 100.0 * achieved / HBM_PEAK_GBS,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                     "kernel": "row_features_kernel", "kernel_ms": avg_ms, "bytes_per_launch": bytes_launch},
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": traffic, **extra},
     }
     if args.copy_probe:
         result["copy_probe"] = copy_probe(torch)
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and batch is not None:
         log("[bench] timing the oracle on the host")
         result["cpu_baseline"] = cpu_baseline(torch, batch, feats, args.cpu_seconds)
         log(f"[bench] oracle {result['cpu_baseline']['value']:.1f} rows/s, "

@@ -26,6 +26,10 @@ HIPCC_FLAGS = [
     "-std=c++17",
     "-fPIC",
     "-Wall",
+    # The row state keeps its exponent reference as a rounded product and
+    # rebases with exact residuals: every fused multiply-add is written out,
+    # the compiler must not form others.
+    "-ffp-contract=off",
     # Keep the compiler from forming packed fp32 instructions.
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", INCLUDE,

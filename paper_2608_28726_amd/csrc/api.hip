@@ -12,9 +12,8 @@ struct pr_stream {
   int device;
   StreamDev dev;
   pr_agg_params params;
-  Partial* ws;         // [max_slots][kStreamMaxSplit]
-  uint32_t* counters;  // [max_slots], zero between launches
-  void* block;         // single allocation backing everything above
+  Partial* ws;  // [max_slots][kStreamMaxSplit]
+  void* block;  // single allocation backing everything above
 };
 
 namespace {
@@ -119,7 +118,7 @@ pr_status pr_token_features(const void* logits, pr_dtype dtype, int64_t n_rows, 
   if (top_p) return hip_status(launch_topp(a, dtype, workspace, as_stream(stream)));
   a.G = row_split(n_rows, vocab, dtype);
   a.ws = static_cast<Partial*>(workspace);
-  return hip_status(launch_row_features(a, dtype, 0, as_stream(stream)));
+  return hip_status(launch_row_features(a, dtype, as_stream(stream)));
 }
 
 pr_status pr_request_aggregate(const pr_token_features_t* feats, const int32_t* offsets, int32_t n_req,
@@ -172,8 +171,7 @@ pr_status pr_stream_create(int32_t max_slots, int32_t max_len, const pr_agg_para
   const size_t b_min = up(S * 4 * sizeof(float));
   const size_t b_cnt = up(S * sizeof(int32_t));
   const size_t b_nan = up(S * sizeof(uint32_t));
-  const size_t b_ctr = up(S * sizeof(uint32_t));
-  const size_t total = b_ws + b_sum + b_hist + b_min + b_cnt + b_nan + b_ctr;
+  const size_t total = b_ws + b_sum + b_hist + b_min + b_cnt + b_nan;
   pr_stream* s = new (std::nothrow) pr_stream();
   if (!s) return PR_ERR_NO_MEMORY;
   hipError_t e = hipGetDevice(&s->device);
@@ -194,13 +192,10 @@ pr_status pr_stream_create(int32_t max_slots, int32_t max_len, const pr_agg_para
   s->dev.count = reinterpret_cast<int32_t*>(b);
   b += b_cnt;
   s->dev.nanbits = reinterpret_cast<uint32_t*>(b);
-  b += b_nan;
-  s->counters = reinterpret_cast<uint32_t*>(b);
   s->dev.max_slots = max_slots;
   s->dev.max_len = max_len;
   s->params = p;
-  e = hipMemset(s->counters, 0, S * sizeof(uint32_t));
-  if (e == hipSuccess) e = launch_stream_clear(s->dev, nullptr, 0, nullptr);
+  e = launch_stream_clear(s->dev, nullptr, 0, nullptr);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
     (void)hipFree(s->block);
@@ -236,10 +231,9 @@ pr_status pr_stream_step(pr_stream* state, const void* logits, pr_dtype dtype, i
   if (G > kStreamMaxSplit) G = kStreamMaxSplit;
   a.G = G;
   a.ws = state->ws;
-  a.counters = state->counters;
   a.slot_ids = slot_ids;
   a.st = state->dev;
-  return hip_status(launch_row_features(a, dtype, 2, as_stream(stream)));
+  return hip_status(launch_row_features(a, dtype, as_stream(stream)));
 }
 
 pr_status pr_stream_finish(pr_stream* state, const int32_t* slots, int32_t n, float threshold,

@@ -66,8 +66,10 @@ struct Elem<uint16_t> {  // bfloat16 bit patterns
 };
 
 // Reduction state of a stretch of one row. S and E are relative to the
-// reference a = m * c (c = log2(e) / T): S = sum 2^x, E = sum 2^x * x with
-// x = z * c - a. t1/t1i/t2: largest value, its lowest index, second value.
+// reference a = round(m * c) (c = log2(e) / T, the float32 product):
+// S = sum 2^x, E = sum 2^x * x with x = fma(z, c, -a). References are always
+// such rounded products and are compared by plain subtraction; the library is
+// built with floating-point contraction off so that this stays so. t1/t1i/t2: largest value, its lowest index, second value.
 // cnt: tokens of the stretch that precede the sampled token in the order.
 struct Partial {
   float m;

@@ -27,8 +27,7 @@ struct RowArgs {
   pr_token_features_t out;  // max_logit == NULL: outputs not written (streaming only)
   int G;                    // workgroups per row
   Partial* ws;              // [n_rows][G] partial states when G > 1
-  uint32_t* counters;       // [n_rows] arrival counters (streaming, G > 1); zero between launches
-  const int32_t* slot_ids;  // streaming only
+  const int32_t* slot_ids;  // streaming only (NULL offline)
   StreamDev st;             // streaming only
 };
 
@@ -36,8 +35,8 @@ struct RowArgs {
 // workspace size query and the launch agree).
 int row_split(int64_t n_rows, int32_t V, pr_dtype dtype);
 
-// mode 0: offline (one kernel when G == 1, partial + merge kernels otherwise);
-// mode 2: streaming step (merge in the last workgroup of each row).
-hipError_t launch_row_features(const RowArgs& a, pr_dtype dtype, int mode, hipStream_t stream);
+// One kernel when G == 1, partial-state and merge kernels otherwise; with
+// slot ids (streaming) each finalised row also updates its request slot.
+hipError_t launch_row_features(const RowArgs& a, pr_dtype dtype, hipStream_t stream);
 
 }  // namespace pr

@@ -11,25 +11,27 @@
 // equal logits by lower index". Comparisons use the raw logits, so
 // temperature scaling cannot create false ties. Lanes merge with wave
 // shuffles, waves through LDS; a row split over G workgroups merges the G
-// partial states either in a second kernel or in the last workgroup to
-// finish (streaming decode).
+// partial states in a second kernel, which also updates the streaming
+// decode state.
 #include "row_scan.h"
 
 namespace pr {
 
 using namespace scan;
 
-// MODE 0: one workgroup per row, finalised in place.
-// MODE 1: G workgroups per row write partial states to a.ws.
-// MODE 2: streaming; G workgroups per row, the last to finish merges,
-//         finalises and updates the request slot.
 // Occupancy target: 8 waves per SIMD keep enough loads in flight.
 #ifndef PR_ROW_WAVES_PER_EU
 #define PR_ROW_WAVES_PER_EU 8
 #endif
 
-template <typename Tin, int BLOCK, int U, int MODE>
-__global__ __launch_bounds__(BLOCK) __attribute__((amdgpu_waves_per_eu(PR_ROW_WAVES_PER_EU)))
+// SPLIT == false: one workgroup per row, finalised in place (and, when
+// slot ids are given, the row's token joins its request slot).
+// SPLIT == true: G workgroups per row write partial states to a.ws; the
+// merge kernel below finalises. Kernel boundaries make the partials visible,
+// so no workgroup waits or fences on another.
+template <typename Tin, int BLOCK, int U, int LD, bool SPLIT>
+__global__ __launch_bounds__(BLOCK)
+__attribute__((amdgpu_waves_per_eu(BLOCK >= 512 ? BLOCK / 256 : PR_ROW_WAVES_PER_EU)))
 void row_features_kernel(RowArgs a) {
   const int G = a.G;
   const int64_t r = blockIdx.x / G;
@@ -44,41 +46,21 @@ void row_features_kernel(RowArgs a) {
 
   Lane L;
   lane_init(L);
-  scan_stretch<Tin, BLOCK, U>(row, a.V, vb, ve, g == 0, g == G - 1, nvec, cx, L);
-  Partial p = block_merge<BLOCK>(L, cx.c);
-
-  __shared__ int sh_last;
-  __shared__ Partial sh_p;
-  if (MODE == 1) {
+  scan_stretch<Tin, BLOCK, U, LD>(row, a.V, vb, ve, g == 0, g == G - 1, nvec, cx, L);
+  const Partial p = block_merge<BLOCK>(L, cx.c);
+  if (SPLIT) {
     if (threadIdx.x == 0) a.ws[r * G + g] = p;
     return;
-  }
-  if (MODE == 2 && G > 1) {
-    if (threadIdx.x == 0) {
-      a.ws[r * G + g] = p;
-      __threadfence();
-      const uint32_t old = atomicAdd(&a.counters[r], 1u);
-      sh_last = (old == static_cast<uint32_t>(G - 1));
-    }
-    __syncthreads();
-    if (!sh_last) return;
-    __threadfence();
-    if (threadIdx.x == 0) {
-      sh_p = merge_partials(a.ws + r * G, G, cx.c);
-      a.counters[r] = 0u;
-    }
-    __syncthreads();
-    p = sh_p;
   }
   const uint32_t fix = rank_fixup<Tin, BLOCK>(row, a.V, nvec, cx);
   if (threadIdx.x == 0) {
     float conf[4];
     finalize_row(a, r, p, cx, fix, conf);
-    if (MODE == 2) stream_update(a.st, a.slot_ids[r], conf);
+    if (a.slot_ids) stream_update(a.st, a.slot_ids[r], conf);
   }
 }
 
-// Second kernel of MODE 1: merges each row's G partials and finalises.
+// Merges each row's G partials in index order and finalises the row.
 template <typename Tin, int BLOCK>
 __global__ __launch_bounds__(BLOCK) void row_merge_kernel(RowArgs a) {
   const int64_t r = blockIdx.x;
@@ -92,6 +74,7 @@ __global__ __launch_bounds__(BLOCK) void row_merge_kernel(RowArgs a) {
     const Partial p = merge_partials(a.ws + r * a.G, a.G, cx.c);
     float conf[4];
     finalize_row(a, r, p, cx, fix, conf);
+    if (a.slot_ids) stream_update(a.st, a.slot_ids[r], conf);
   }
 }
 
@@ -108,7 +91,6 @@ namespace {
 #endif
 
 constexpr int kBlock = PR_ROW_BLOCK;
-constexpr int kTargetBlocks = 2048;  // 8 workgroups per CU on 256 CUs
 constexpr int kMaxSplit = 64;
 
 // 16-byte vectors per lane per loop step.
@@ -119,36 +101,55 @@ constexpr int unroll_for() {
 
 }  // namespace
 
+#ifndef PR_WIDE_ROWS
+#define PR_WIDE_ROWS 2048
+#endif
+#ifndef PR_WIDE_BLOCK
+#define PR_WIDE_BLOCK 1024
+#endif
+// Below this many rows a row gets one wide workgroup (or several, split),
+// so that small batches need a single launch and still fill the chip.
+constexpr int64_t kWideRows = PR_WIDE_ROWS;
+constexpr int kWideBlock = PR_WIDE_BLOCK;
+constexpr int kWideTarget = 256;  // wide workgroups per launch: one per CU
+
 int row_split(int64_t n_rows, int32_t V, pr_dtype dtype) {
   const int VEC = dtype == PR_BF16 ? 8 : 4;
   const int64_t nvec = V / VEC;
-  if (n_rows <= 0 || n_rows >= kTargetBlocks) return 1;
-  int64_t G = (kTargetBlocks + n_rows - 1) / n_rows;
-  const int64_t by_work = nvec / (kBlock * 4);  // at least ~4 vectors per lane
+  if (n_rows <= 0 || n_rows >= kWideTarget) return 1;
+  int64_t G = (kWideTarget + n_rows - 1) / n_rows;
+  const int64_t by_work = nvec / (kWideBlock * 4);  // at least ~4 vectors per lane
   if (G > by_work) G = by_work;
   if (G > kMaxSplit) G = kMaxSplit;
   if (G < 1) G = 1;
   return static_cast<int>(G);
 }
 
+#ifndef PR_WIDE_LOAD_DEPTH
+#define PR_WIDE_LOAD_DEPTH 4
+#endif
+
 template <typename Tin>
-static hipError_t launch_typed(const RowArgs& a, int mode, hipStream_t stream) {
+static hipError_t launch_typed(const RowArgs& a, hipStream_t stream) {
   constexpr int U = unroll_for<Tin>();
+  // Wide workgroups serve small batches, where each lane has few vectors:
+  // they keep many loads in flight so that few memory latencies add up.
+  constexpr int LDW = PR_WIDE_LOAD_DEPTH;
   const dim3 grid(static_cast<unsigned>(a.n_rows * a.G));
-  if (mode == 2) {
-    row_features_kernel<Tin, kBlock, U, 2><<<grid, kBlock, 0, stream>>>(a);
+  if (a.n_rows >= kWideRows) {
+    row_features_kernel<Tin, kBlock, U, U, false><<<grid, kBlock, 0, stream>>>(a);
   } else if (a.G == 1) {
-    row_features_kernel<Tin, kBlock, U, 0><<<grid, kBlock, 0, stream>>>(a);
+    row_features_kernel<Tin, kWideBlock, U, LDW, false><<<grid, kWideBlock, 0, stream>>>(a);
   } else {
-    row_features_kernel<Tin, kBlock, U, 1><<<grid, kBlock, 0, stream>>>(a);
+    row_features_kernel<Tin, kWideBlock, U, LDW, true><<<grid, kWideBlock, 0, stream>>>(a);
     row_merge_kernel<Tin, kWave><<<dim3(static_cast<unsigned>(a.n_rows)), kWave, 0, stream>>>(a);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_row_features(const RowArgs& a, pr_dtype dtype, int mode, hipStream_t stream) {
+hipError_t launch_row_features(const RowArgs& a, pr_dtype dtype, hipStream_t stream) {
   if (a.n_rows == 0) return hipSuccess;
-  return dtype == PR_BF16 ? launch_typed<uint16_t>(a, mode, stream) : launch_typed<float>(a, mode, stream);
+  return dtype == PR_BF16 ? launch_typed<uint16_t>(a, stream) : launch_typed<float>(a, stream);
 }
 
 }  // namespace pr

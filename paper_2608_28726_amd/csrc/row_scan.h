@@ -57,7 +57,7 @@ __device__ __forceinline__ void lane_rescale(Lane& L, float m_new, float c) {
 // of the wave calls this together (wave-uniform control flow), so the
 // cross-lane steps below see all 64 lanes.
 template <typename Tin, int NV, int BLOCK>
-__device__ __forceinline__ void consume(const uint4 (&v)[NV], int64_t i, const RowCtx& cx, Lane& L) {
+__device__ __forceinline__ void consume(const uint4* v, int64_t i, const RowCtx& cx, Lane& L) {
   constexpr int VEC = Elem<Tin>::kVec;
   float z[NV * VEC];
 #pragma unroll
@@ -265,8 +265,6 @@ __device__ __forceinline__ uint4 load_stream(const uint4* p) {
 #endif
 }
 
-// Scan of the vector index range [vb, ve) of one row by one workgroup,
-// plus the scalar head (first) / tail (last) elements.
 // All-(-inf) vector: padding for lanes past the end of a stretch.
 template <typename Tin>
 __device__ __forceinline__ uint4 neg_inf_vec() {
@@ -275,13 +273,15 @@ __device__ __forceinline__ uint4 neg_inf_vec() {
 }
 
 // Scan of the vector index range [vb, ve) of one row by one workgroup,
-// plus the scalar head (first) / tail (last) elements. Loop trip counts are
-// uniform across each wave: full steps while the wave's last lane still has
-// U vectors, then single-vector steps in which lanes past the end see -inf
+// plus the scalar head (first) / tail (last) elements. Each lane keeps LD
+// 16-byte loads in flight and reduces them U at a time. Loop trip counts are
+// uniform across each wave: full rounds while the wave's last lane still has
+// LD vectors, then one predicated round in which lanes past the end see -inf
 // (a token of probability 0 that changes no result).
-template <typename Tin, int BLOCK, int U>
+template <typename Tin, int BLOCK, int U, int LD>
 __device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve, bool do_head, bool do_tail,
                              int64_t nvec, const RowCtx& cx, Lane& L) {
+  static_assert(LD % U == 0, "load depth must be a multiple of the compute width");
   constexpr int VEC = Elem<Tin>::kVec;
   const Tin* base = static_cast<const Tin*>(row) + cx.h;
   const uint4* vp = reinterpret_cast<const uint4*>(base);
@@ -294,16 +294,22 @@ __device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve,
   }
   int64_t i = vb + t;
   int64_t i_last = vb + wave_first + (kWave - 1);  // the wave's last lane
-  for (; i_last + (U - 1) * BLOCK < ve; i += U * BLOCK, i_last += U * BLOCK) {
-    uint4 v[U];
+  for (; i_last + (LD - 1) * BLOCK < ve; i += LD * BLOCK, i_last += LD * BLOCK) {
+    uint4 v[LD];
 #pragma unroll
-    for (int u = 0; u < U; ++u) v[u] = load_stream(vp + i + u * BLOCK);
-    consume<Tin, U, BLOCK>(v, i, cx, L);
+    for (int u = 0; u < LD; ++u) v[u] = load_stream(vp + i + u * BLOCK);
+#pragma unroll
+    for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK>(v + c, i + c * BLOCK, cx, L);
   }
-  for (int64_t i_first = i - __lane_id(); i_first < ve; i += BLOCK, i_first += BLOCK) {
-    uint4 v[1];
-    v[0] = i < ve ? load_stream(vp + i) : neg_inf_vec<Tin>();
-    consume<Tin, 1, BLOCK>(v, i, cx, L);
+  if (i - static_cast<int64_t>(__lane_id()) < ve) {  // the wave's first lane has vectors left
+    uint4 v[LD];
+#pragma unroll
+    for (int u = 0; u < LD; ++u) {
+      const int64_t j = i + u * BLOCK;
+      v[u] = j < ve ? load_stream(vp + j) : neg_inf_vec<Tin>();
+    }
+#pragma unroll
+    for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK>(v + c, i + c * BLOCK, cx, L);
   }
   if (do_tail) {
     const int64_t tail0 = cx.h + nvec * VEC;

@@ -235,7 +235,7 @@ __global__ __launch_bounds__(kTpBlock) void topp_kernel(RowArgs a) {
   // 1. stats pass
   Lane L;
   lane_init(L);
-  scan_stretch<Tin, kTpBlock, 2>(row, a.V, 0, nvec, true, true, nvec, cx, L);
+  scan_stretch<Tin, kTpBlock, 2, 8>(row, a.V, 0, nvec, true, true, nvec, cx, L);
   Partial p = block_merge<kTpBlock>(L, cx.c);
   const uint32_t fix = rank_fixup<Tin, kTpBlock>(row, a.V, nvec, cx);
   if (threadIdx.x == 0) {
