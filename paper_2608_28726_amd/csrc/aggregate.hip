@@ -61,13 +61,13 @@ __device__ void wave_stats(Get get, int64_t lo, int64_t n, double& sum, float& m
   has_nan = wave_sum_u(nan) != 0;
 }
 
-// The j-th smallest (1-based) of each wave's n values, by a byte-wise radix
-// select over order-preserving keys: per pass a 256-bin histogram of the
-// keys that match the digits chosen so far, then a wave prefix scan locates
-// the bin holding the j-th key. Every wave of the block must call this with
-// the same n (it uses block barriers). hist: [4][256], sel: [4][2] in LDS.
-template <typename Get>
-__device__ float radix_select(Get get, int64_t lo, int64_t n, int64_t j, uint32_t* hist, uint32_t* sel) {
+// Byte-wise radix select of the j-th smallest (1-based) key: per pass a
+// 256-bin histogram of the keys that match the digits chosen so far, then a
+// wave prefix scan locates the bin holding the j-th key. Every wave of the
+// block must call this with the same n (it uses block barriers).
+// hist: [4][256], sel: [4][2] in LDS. keys(k) yields the k-th key.
+template <typename Keys>
+__device__ uint32_t radix_select_keys(Keys keys, int64_t n, int64_t j, uint32_t* hist, uint32_t* sel) {
   const int w = threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
   uint32_t* h = hist + w * 256;
@@ -76,10 +76,9 @@ __device__ float radix_select(Get get, int64_t lo, int64_t n, int64_t j, uint32_
     const int shift = 24 - 8 * pass;
     for (int b = lane; b < 256; b += kWave) h[b] = 0;
     __syncthreads();
-    for (int64_t k = lane; k < n; k += kWave) {
-      const uint32_t key = float_key(get(lo + k));
+    keys.for_each([&](uint32_t key) {
       if ((key & mask) == prefix) atomicAdd(&h[(key >> shift) & 255u], 1u);
-    }
+    });
     __syncthreads();
     const uint32_t c0 = h[4 * lane], c1 = h[4 * lane + 1], c2 = h[4 * lane + 2], c3 = h[4 * lane + 3];
     const uint32_t tot = c0 + c1 + c2 + c3;
@@ -107,7 +106,51 @@ __device__ float radix_select(Get get, int64_t lo, int64_t n, int64_t j, uint32_
     need = sel[2 * w + 1];
     mask |= 255u << shift;
   }
-  return key_float(prefix);
+  return prefix;
+}
+
+// Keys read from memory on every pass (any n).
+template <typename Get>
+struct MemKeys {
+  Get get;
+  int64_t lo, n;
+  template <typename Fn>
+  __device__ __forceinline__ void for_each(Fn fn) const {
+    for (int64_t k = threadIdx.x % kWave; k < n; k += kWave) fn(float_key(get(lo + k)));
+  }
+};
+
+// Keys held in registers, R per lane (n <= R * 64): one read for all passes.
+template <int R>
+struct RegKeys {
+  uint32_t k[R];
+  int cnt;  // keys this lane holds
+  template <typename Fn>
+  __device__ __forceinline__ void for_each(Fn fn) const {
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      if (r < cnt) fn(k[r]);
+  }
+};
+
+constexpr int kRegKeys = 16;  // up to 1,024 values per column stay in registers
+
+// The j-th smallest of the wave's n values get(lo + k).
+template <typename Get>
+__device__ float radix_select(Get get, int64_t lo, int64_t n, int64_t j, uint32_t* hist, uint32_t* sel) {
+  if (n <= static_cast<int64_t>(kRegKeys) * kWave) {
+    RegKeys<kRegKeys> rk;
+    rk.cnt = 0;
+    const int lane = threadIdx.x % kWave;
+#pragma unroll
+    for (int r = 0; r < kRegKeys; ++r) {
+      const int64_t k = lane + static_cast<int64_t>(r) * kWave;
+      rk.k[r] = k < n ? float_key(get(lo + k)) : 0u;
+      rk.cnt += k < n ? 1 : 0;
+    }
+    return key_float(radix_select_keys(rk, n, j, hist, sel));
+  }
+  return key_float(radix_select_keys(MemKeys<Get>{get, lo, n}, n, j, hist, sel));
 }
 
 __device__ int64_t quant_rank(double q, int64_t n) {

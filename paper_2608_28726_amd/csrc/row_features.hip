@@ -19,9 +19,10 @@ namespace pr {
 
 using namespace scan;
 
-// Occupancy target: 8 waves per SIMD keep enough loads in flight.
+// Occupancy target: 6 waves per SIMD keep enough loads in flight and leave
+// the registers the rarely taken top-2 tournament needs without spilling.
 #ifndef PR_ROW_WAVES_PER_EU
-#define PR_ROW_WAVES_PER_EU 8
+#define PR_ROW_WAVES_PER_EU 6
 #endif
 
 // SPLIT == false: one workgroup per row, finalised in place (and, when
@@ -117,7 +118,7 @@ int row_split(int64_t n_rows, int32_t V, pr_dtype dtype) {
   const int VEC = dtype == PR_BF16 ? 8 : 4;
   const int64_t nvec = V / VEC;
   if (n_rows <= 0 || n_rows >= kWideTarget) return 1;
-  int64_t G = (kWideTarget + n_rows - 1) / n_rows;
+  int64_t G = kWideTarget / n_rows;  // one round of at most kWideTarget workgroups
   const int64_t by_work = nvec / (kWideBlock * 4);  // at least ~4 vectors per lane
   if (G > by_work) G = by_work;
   if (G > kMaxSplit) G = kMaxSplit;

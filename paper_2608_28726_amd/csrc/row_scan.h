@@ -14,7 +14,8 @@ struct Lane {
   float S0, S1;    // two accumulators of sum 2^x (alternating elements)
   float E0, E1;    // two accumulators of sum 2^x * x
   float t1, t2;    // largest and second value this lane recorded
-  int32_t t1i;     // index of t1 (lowest among ties)
+  int32_t t1i;     // index of t1 (lowest among ties), once known
+  int32_t t1v;     // first vector index of the step where t1 was set (-1: t1i is exact)
   uint32_t cnt;    // rank counts (ballot totals are added in lane 0 only)
   float thr2;      // wave-uniform: max over the wave's lanes of t2
 };
@@ -35,6 +36,7 @@ __device__ __forceinline__ void lane_init(Lane& L) {
   L.t1 = -INFINITY;
   L.t2 = -INFINITY;
   L.t1i = kNoIndex;
+  L.t1v = -1;
   L.cnt = 0;
   L.thr2 = -INFINITY;
 }
@@ -51,6 +53,30 @@ __device__ __forceinline__ void lane_rescale(Lane& L, float m_new, float c) {
   L.S0 *= s;
   L.S1 *= s;
   L.a = a_new;
+}
+
+// Largest and second largest of N values (duplicates count), by a pairwise
+// tournament: leaves keep (max, min) of pairs, merges keep
+// (max of maxima, max of the smaller maximum and both seconds).
+template <int N>
+__device__ __forceinline__ void top2_of(const float* z, float& c1, float& c2) {
+  float h[N / 2], s2[N / 2];
+#pragma unroll
+  for (int k = 0; k < N / 2; ++k) {
+    h[k] = fmaxf(z[2 * k], z[2 * k + 1]);
+    s2[k] = fminf(z[2 * k], z[2 * k + 1]);
+  }
+#pragma unroll
+  for (int w = N / 2; w > 1; w >>= 1) {
+#pragma unroll
+    for (int k = 0; k < w / 2; ++k) {
+      const float a = h[2 * k], b = h[2 * k + 1];
+      s2[k] = fmaxf(fminf(a, b), fmaxf(s2[2 * k], s2[2 * k + 1]));
+      h[k] = fmaxf(a, b);
+    }
+  }
+  c1 = h[0];
+  c2 = s2[0];
 }
 
 // NV vectors of one lane; vector u has vector index i + u * BLOCK. Every lane
@@ -70,30 +96,6 @@ __device__ __forceinline__ void consume(const uint4* v, int64_t i, const RowCtx&
   // The wave shares one reference, its running maximum: every exponent
   // argument stays <= 0 and the reference moves only on a new wave maximum.
   if (__any(cmax > L.mw)) lane_rescale(L, wave_max(cmax), cx.c);
-
-  // Top-1/top-2. An element no larger than thr2 cannot change the row's
-  // result: some lane already holds two values >= it at lower indices (every
-  // chunk lies above the previous ones in index order). thr2 rises quickly,
-  // so the per-element update below runs on few chunks.
-  if (__any(cmax > L.thr2)) {
-    if (cmax > L.t2) {
-#pragma unroll
-      for (int u = 0; u < NV; ++u) {
-#pragma unroll
-        for (int k = 0; k < VEC; ++k) {
-          const float zk = z[u * VEC + k];
-          if (zk > L.t1) {
-            L.t2 = L.t1;
-            L.t1 = zk;
-            L.t1i = static_cast<int32_t>(cx.h + (i + u * BLOCK) * VEC + k);
-          } else if (zk > L.t2) {
-            L.t2 = zk;
-          }
-        }
-      }
-    }
-    L.thr2 = wave_max(L.t2);
-  }
 
   // Rank of y: a vector wholly before y counts z >= z_y (z > next_below(z_y)),
   // any other vector counts z > z_y; ties before y inside y's own vector are
@@ -124,6 +126,25 @@ __device__ __forceinline__ void consume(const uint4* v, int64_t i, const RowCtx&
     L.E0 = fmaf(e0, fmaxf(x0, -kBig), L.E0);
     L.E1 = fmaf(e1, fmaxf(x1, -kBig), L.E1);
   }
+
+  // Top-1/top-2 values. An element no larger than thr2 cannot change the
+  // row's result: some lane already holds two values >= it at lower indices
+  // (every step lies above the previous ones in index order). thr2 rises
+  // quickly, so the update below runs on few steps; it takes the step's own
+  // top two values by a pairwise tournament and merges them into the lane's.
+  // Where t1 rises, only the step is recorded; its exact index is found once
+  // the stretch is done (recover_argmax).
+  if (__any(cmax > L.thr2)) {
+    float c1, c2;
+    top2_of<NV * VEC>(z, c1, c2);  // last use of z: may reuse its registers
+    L.t2 = fmaxf(fmaxf(L.t2, c2), fminf(L.t1, c1));
+    if (c1 > L.t1) {
+      L.t1 = c1;
+      L.t1v = static_cast<int32_t>(i);
+    }
+    L.thr2 = wave_max(L.t2);
+  }
+
 }
 
 // One element outside the aligned vectors (row head or tail), per lane.
@@ -133,6 +154,7 @@ __device__ __forceinline__ void consume_scalar(float z, int64_t idx, const RowCt
     L.t2 = L.t1;
     L.t1 = z;
     L.t1i = static_cast<int32_t>(idx);
+    L.t1v = -1;
   } else if (z > L.t2) {
     L.t2 = z;
   }
@@ -314,6 +336,23 @@ __device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve,
   if (do_tail) {
     const int64_t tail0 = cx.h + nvec * VEC;
     for (int64_t e = tail0 + t; e < V; e += BLOCK) consume_scalar(Elem<Tin>::load1(row, e), e, cx, L);
+  }
+  // Exact index of the wave maximum: the lanes holding it re-read the step
+  // where their t1 was set and take its first occurrence (a few bytes per
+  // wave; ties across lanes and waves resolve by index in the merges).
+  const float mw = wave_max(L.t1);
+  if (L.t1 == mw && L.t1v >= 0) {
+    int32_t best = kNoIndex;
+    for (int u = U - 1; u >= 0; --u) {
+      const int64_t j = static_cast<int64_t>(L.t1v) + u * BLOCK;
+      if (j >= ve) continue;
+      float z[VEC];
+      Elem<Tin>::unpack(vp[j], z);
+#pragma unroll
+      for (int k = VEC - 1; k >= 0; --k)
+        if (z[k] == mw) best = static_cast<int32_t>(cx.h + j * VEC + k);
+    }
+    L.t1i = best;
   }
 }
 
