@@ -29,6 +29,11 @@ __device__ __forceinline__ float next_below(float x) {
   return __uint_as_float((b & 0x80000000u) ? b + 1u : b - 1u);
 }
 
+// A 16-byte vector of logits as four 32-bit words. A native vector type
+// keeps each load in one register quadruple, so loads carried across loop
+// iterations need no register copies (which would wait for the load).
+typedef uint32_t vec4u __attribute__((ext_vector_type(4)));
+
 // Element access: a 16-byte vector holds 4 float32 or 8 bfloat16 logits.
 template <typename Tin>
 struct Elem;
@@ -36,7 +41,7 @@ struct Elem;
 template <>
 struct Elem<float> {
   static constexpr int kVec = 4;
-  __device__ __forceinline__ static void unpack(const uint4& v, float* z) {
+  __device__ __forceinline__ static void unpack(const vec4u& v, float* z) {
     z[0] = __uint_as_float(v.x);
     z[1] = __uint_as_float(v.y);
     z[2] = __uint_as_float(v.z);
@@ -50,7 +55,7 @@ struct Elem<float> {
 template <>
 struct Elem<uint16_t> {  // bfloat16 bit patterns
   static constexpr int kVec = 8;
-  __device__ __forceinline__ static void unpack(const uint4& v, float* z) {
+  __device__ __forceinline__ static void unpack(const vec4u& v, float* z) {
     z[0] = bf16_lo(v.x);
     z[1] = bf16_hi(v.x);
     z[2] = bf16_lo(v.y);
@@ -82,28 +87,114 @@ struct Partial {
   uint32_t pad;
 };
 
+// Wave-wide reductions by DPP lane moves within the wave (no LDS round
+// trips): two quad permutations, the half-row and row mirrors combine the 16
+// lanes of each row, the row broadcasts of lanes 15 and 31 fold the four rows
+// into lane 63, whose value every lane then reads as a scalar. Each must be
+// called with all 64 lanes active.
+namespace dpp {
+constexpr int kXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kHalfMirror = 0x141;  // row_half_mirror
+constexpr int kMirror = 0x140;      // row_mirror
+constexpr int kBcast15 = 0x142;     // row_bcast:15 (rows 1 and 3 written)
+constexpr int kBcast31 = 0x143;     // row_bcast:31 (rows 2 and 3 written)
+
+// src moved by CTRL; lanes of rows outside ROW_MASK receive `old`.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ uint32_t mov(uint32_t old, uint32_t src) {
+  return static_cast<uint32_t>(
+      __builtin_amdgcn_update_dpp(static_cast<int>(old), static_cast<int>(src), CTRL, ROW_MASK, 0xf, false));
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float movf(float old, float src) {
+  return __uint_as_float(mov<CTRL, ROW_MASK>(__float_as_uint(old), __float_as_uint(src)));
+}
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double movd(double old, double src) {
+  const uint64_t o = __double_as_longlong(old), v = __double_as_longlong(src);
+  const uint32_t lo = mov<CTRL, ROW_MASK>(static_cast<uint32_t>(o), static_cast<uint32_t>(v));
+  const uint32_t hi = mov<CTRL, ROW_MASK>(static_cast<uint32_t>(o >> 32), static_cast<uint32_t>(v >> 32));
+  return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
+}
+__device__ __forceinline__ float lane63(float v) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), kWave - 1));
+}
+__device__ __forceinline__ uint32_t lane63(uint32_t v) {
+  return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), kWave - 1));
+}
+__device__ __forceinline__ int32_t lane63(int32_t v) { return __builtin_amdgcn_readlane(v, kWave - 1); }
+__device__ __forceinline__ double lane63(double v) {
+  const uint64_t b = __double_as_longlong(v);
+  const uint32_t lo = lane63(static_cast<uint32_t>(b)), hi = lane63(static_cast<uint32_t>(b >> 32));
+  return __longlong_as_double(static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo));
+}
+}  // namespace dpp
+
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = kWave / 2; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+  using namespace dpp;
+  v = fmaxf(v, movf<kXor1, 0xf>(v, v));
+  v = fmaxf(v, movf<kXor2, 0xf>(v, v));
+  v = fmaxf(v, movf<kHalfMirror, 0xf>(v, v));
+  v = fmaxf(v, movf<kMirror, 0xf>(v, v));
+  v = fmaxf(v, movf<kBcast15, 0xa>(v, v));
+  v = fmaxf(v, movf<kBcast31, 0xc>(v, v));
+  return lane63(v);
 }
 
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  using namespace dpp;
+  v += movf<kXor1, 0xf>(0.0f, v);
+  v += movf<kXor2, 0xf>(0.0f, v);
+  v += movf<kHalfMirror, 0xf>(0.0f, v);
+  v += movf<kMirror, 0xf>(0.0f, v);
+  v += movf<kBcast15, 0xa>(0.0f, v);
+  v += movf<kBcast31, 0xc>(0.0f, v);
+  return lane63(v);
 }
 
 __device__ __forceinline__ double wave_sum_d(double v) {
-#pragma unroll
-  for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  using namespace dpp;
+  v += movd<kXor1, 0xf>(0.0, v);
+  v += movd<kXor2, 0xf>(0.0, v);
+  v += movd<kHalfMirror, 0xf>(0.0, v);
+  v += movd<kMirror, 0xf>(0.0, v);
+  v += movd<kBcast15, 0xa>(0.0, v);
+  v += movd<kBcast31, 0xc>(0.0, v);
+  return lane63(v);
 }
 
 __device__ __forceinline__ uint32_t wave_sum_u(uint32_t v) {
-#pragma unroll
-  for (int o = kWave / 2; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  using namespace dpp;
+  v += mov<kXor1, 0xf>(0u, v);
+  v += mov<kXor2, 0xf>(0u, v);
+  v += mov<kHalfMirror, 0xf>(0u, v);
+  v += mov<kMirror, 0xf>(0u, v);
+  v += mov<kBcast15, 0xa>(0u, v);
+  v += mov<kBcast31, 0xc>(0u, v);
+  return lane63(v);
+}
+
+// Largest and second value of the multiset of all lanes' (a1, a2) pairs
+// (a1 >= a2 in every lane); the result is in every lane.
+__device__ __forceinline__ void wave_top2_values(float& a1, float& a2) {
+  using namespace dpp;
+#define PR_TOP2_STEP(CTRL, MASK)                                           \
+  {                                                                        \
+    const float o1 = movf<CTRL, MASK>(-INFINITY, a1);                      \
+    const float o2 = movf<CTRL, MASK>(-INFINITY, a2);                      \
+    a2 = fmaxf(fminf(a1, o1), fmaxf(a2, o2));                              \
+    a1 = fmaxf(a1, o1);                                                    \
+  }
+  PR_TOP2_STEP(kXor1, 0xf)
+  PR_TOP2_STEP(kXor2, 0xf)
+  PR_TOP2_STEP(kHalfMirror, 0xf)
+  PR_TOP2_STEP(kMirror, 0xf)
+  PR_TOP2_STEP(kBcast15, 0xa)
+  PR_TOP2_STEP(kBcast31, 0xc)
+#undef PR_TOP2_STEP
+  a1 = lane63(a1);
+  a2 = lane63(a2);
 }
 
 // (t1, t1i, t2) merge: larger value first, equal values by lower index; the
@@ -119,13 +210,25 @@ __device__ __forceinline__ void top2_merge(float& t1, int32_t& t1i, float& t2, f
 }
 
 __device__ __forceinline__ void wave_top2(float& t1, int32_t& t1i, float& t2) {
-#pragma unroll
-  for (int o = kWave / 2; o > 0; o >>= 1) {
-    const float o1 = __shfl_xor(t1, o);
-    const int32_t o1i = __shfl_xor(t1i, o);
-    const float o2 = __shfl_xor(t2, o);
-    top2_merge(t1, t1i, t2, o1, o1i, o2);
+  using namespace dpp;
+#define PR_TOP2I_STEP(CTRL, MASK)                                                             \
+  {                                                                                           \
+    const float o1 = movf<CTRL, MASK>(-INFINITY, t1);                                         \
+    const int32_t o1i = static_cast<int32_t>(mov<CTRL, MASK>(static_cast<uint32_t>(kNoIndex), \
+                                                             static_cast<uint32_t>(t1i)));    \
+    const float o2 = movf<CTRL, MASK>(-INFINITY, t2);                                         \
+    top2_merge(t1, t1i, t2, o1, o1i, o2);                                                     \
   }
+  PR_TOP2I_STEP(kXor1, 0xf)
+  PR_TOP2I_STEP(kXor2, 0xf)
+  PR_TOP2I_STEP(kHalfMirror, 0xf)
+  PR_TOP2I_STEP(kMirror, 0xf)
+  PR_TOP2I_STEP(kBcast15, 0xa)
+  PR_TOP2I_STEP(kBcast31, 0xc)
+#undef PR_TOP2I_STEP
+  t1 = dpp::lane63(t1);
+  t1i = dpp::lane63(t1i);
+  t2 = dpp::lane63(t2);
 }
 
 // Rescale factor from a stretch's reference a_l to the row reference A.

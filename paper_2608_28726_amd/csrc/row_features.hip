@@ -19,10 +19,11 @@ namespace pr {
 
 using namespace scan;
 
-// Occupancy target: 6 waves per SIMD keep enough loads in flight and leave
-// the registers the rarely taken top-2 tournament needs without spilling.
+// Occupancy target of the one-row-per-workgroup kernel: 5 waves per SIMD
+// leave the registers of two load buffers and the rarely taken top-2
+// tournament without spilling.
 #ifndef PR_ROW_WAVES_PER_EU
-#define PR_ROW_WAVES_PER_EU 6
+#define PR_ROW_WAVES_PER_EU 5
 #endif
 
 // SPLIT == false: one workgroup per row, finalised in place (and, when
@@ -40,14 +41,23 @@ void row_features_kernel(RowArgs a) {
   if (r >= a.n_rows) return;
   constexpr int VEC = Elem<Tin>::kVec;
   const void* row = static_cast<const Tin*>(a.logits) + r * a.row_stride;
-  const RowCtx cx = row_ctx<Tin>(a, r, row);
-  const int64_t nvec = (a.V - cx.h) / VEC;
+  const int64_t h = head_elems<Tin>(row, a.V);
+  const int64_t nvec = (a.V - h) / VEC;
   const int64_t vb = nvec * g / G;
   const int64_t ve = nvec * (g + 1) / G;
+  vec4u v[LD];
+  stretch_prefetch<Tin, BLOCK, LD>(row, h, vb, ve, v);
+  const RowCtx cx = row_ctx<Tin>(a, r, row);
+  // Wide workgroups (one row per CU) read the slot state early so that its
+  // latency hides behind the row; narrow ones read it at the end, where
+  // other workgroups on the CU cover it and no registers stay tied up.
+  constexpr bool kEarlySlot = !SPLIT && BLOCK >= 512;
+  SlotState ss{-1};
+  if (kEarlySlot) ss = slot_load(a, r);
 
   Lane L;
   lane_init(L);
-  scan_stretch<Tin, BLOCK, U, LD>(row, a.V, vb, ve, g == 0, g == G - 1, nvec, cx, L);
+  scan_stretch<Tin, BLOCK, U, LD>(row, a.V, vb, ve, g == 0, g == G - 1, nvec, cx, L, v);
   const Partial p = block_merge<BLOCK>(L, cx.c);
   if (SPLIT) {
     if (threadIdx.x == 0) a.ws[r * G + g] = p;
@@ -57,7 +67,7 @@ void row_features_kernel(RowArgs a) {
   if (threadIdx.x == 0) {
     float conf[4];
     finalize_row(a, r, p, cx, fix, conf);
-    if (a.slot_ids) stream_update(a.st, a.slot_ids[r], conf);
+    stream_update(a.st, kEarlySlot ? ss : slot_load(a, r), conf);
   }
 }
 
@@ -70,12 +80,13 @@ __global__ __launch_bounds__(BLOCK) void row_merge_kernel(RowArgs a) {
   const void* row = static_cast<const Tin*>(a.logits) + r * a.row_stride;
   const RowCtx cx = row_ctx<Tin>(a, r, row);
   const int64_t nvec = (a.V - cx.h) / VEC;
+  const SlotState ss = slot_load(a, r);
   const uint32_t fix = rank_fixup<Tin, BLOCK>(row, a.V, nvec, cx);
   if (threadIdx.x == 0) {
     const Partial p = merge_partials(a.ws + r * a.G, a.G, cx.c);
     float conf[4];
     finalize_row(a, r, p, cx, fix, conf);
-    if (a.slot_ids) stream_update(a.st, a.slot_ids[r], conf);
+    stream_update(a.st, ss, conf);
   }
 }
 
@@ -90,6 +101,14 @@ namespace {
 #ifndef PR_UNROLL_F32
 #define PR_UNROLL_F32 4
 #endif
+// Load depth LD of the one-row-per-workgroup kernel: with double buffering
+// each lane keeps between LD and 2 * LD 16-byte loads in flight.
+#ifndef PR_LOAD_DEPTH_BF16
+#define PR_LOAD_DEPTH_BF16 2
+#endif
+#ifndef PR_LOAD_DEPTH_F32
+#define PR_LOAD_DEPTH_F32 4
+#endif
 
 constexpr int kBlock = PR_ROW_BLOCK;
 constexpr int kMaxSplit = 64;
@@ -98,6 +117,10 @@ constexpr int kMaxSplit = 64;
 template <typename Tin>
 constexpr int unroll_for() {
   return Elem<Tin>::kVec == 8 ? PR_UNROLL_BF16 : PR_UNROLL_F32;
+}
+template <typename Tin>
+constexpr int load_depth_for() {
+  return Elem<Tin>::kVec == 8 ? PR_LOAD_DEPTH_BF16 : PR_LOAD_DEPTH_F32;
 }
 
 }  // namespace
@@ -126,19 +149,24 @@ int row_split(int64_t n_rows, int32_t V, pr_dtype dtype) {
   return static_cast<int>(G);
 }
 
-#ifndef PR_WIDE_LOAD_DEPTH
-#define PR_WIDE_LOAD_DEPTH 4
+#ifndef PR_WIDE_LOAD_DEPTH_BF16
+#define PR_WIDE_LOAD_DEPTH_BF16 2
+#endif
+#ifndef PR_WIDE_LOAD_DEPTH_F32
+#define PR_WIDE_LOAD_DEPTH_F32 4
 #endif
 
 template <typename Tin>
 static hipError_t launch_typed(const RowArgs& a, hipStream_t stream) {
   constexpr int U = unroll_for<Tin>();
-  // Wide workgroups serve small batches, where each lane has few vectors:
-  // they keep many loads in flight so that few memory latencies add up.
-  constexpr int LDW = PR_WIDE_LOAD_DEPTH;
+  constexpr int LD = load_depth_for<Tin>();
+  // Wide workgroups serve small batches, where each lane has few vectors; 16
+  // waves per CU keep the loads in flight, so a shallow per-lane pipeline
+  // (less padding in the last rounds) serves them best.
+  constexpr int LDW = Elem<Tin>::kVec == 8 ? PR_WIDE_LOAD_DEPTH_BF16 : PR_WIDE_LOAD_DEPTH_F32;
   const dim3 grid(static_cast<unsigned>(a.n_rows * a.G));
   if (a.n_rows >= kWideRows) {
-    row_features_kernel<Tin, kBlock, U, U, false><<<grid, kBlock, 0, stream>>>(a);
+    row_features_kernel<Tin, kBlock, U, LD, false><<<grid, kBlock, 0, stream>>>(a);
   } else if (a.G == 1) {
     row_features_kernel<Tin, kWideBlock, U, LDW, false><<<grid, kWideBlock, 0, stream>>>(a);
   } else {

@@ -21,13 +21,39 @@ struct Lane {
 };
 
 struct RowCtx {
+  float T;           // temperature of the row
   float c;           // log2(e) / T
   float zy;          // logit of the sampled token (NaN when y is invalid)
   float thr_before;  // strict threshold for vectors wholly before y
   float thr_lo;      // min of the two thresholds: lazy-skip test
   int32_t y;         // sampled id, or -1 when invalid
+  uint32_t fix_vec;  // logits equal to z_y before y inside y's own vector
   int64_t h;         // scalar head elements before the first aligned vector
 };
+
+// A value shared by the waves of a workgroup while they scan one stretch,
+// as a sortable key updated by LDS atomic max: the largest value v such that
+// some wave holds two logits >= v (a skip threshold for the top-2 update).
+// It only decides which steps take the exact update, so results do not
+// depend on the order of the atomics; a stale read only makes a wave more
+// conservative. (The exponent sums keep per-wave references: a shared one
+// would make their rounding depend on timing.)
+struct ScanBlock {
+  uint32_t second_key;
+};
+
+__device__ __forceinline__ ScanBlock& scan_block() {
+  __shared__ ScanBlock sb;
+  return sb;
+}
+
+// Publishes v and returns the largest value published so far (v included).
+__device__ __forceinline__ float block_share_max(uint32_t* slot, float v) {
+  uint32_t old = 0;
+  if (__lane_id() == 0) old = atomicMax(slot, float_key(v));
+  old = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(old)));
+  return fmaxf(v, key_float(old));
+}
 
 __device__ __forceinline__ void lane_init(Lane& L) {
   L.mw = -INFINITY;
@@ -83,7 +109,7 @@ __device__ __forceinline__ void top2_of(const float* z, float& c1, float& c2) {
 // of the wave calls this together (wave-uniform control flow), so the
 // cross-lane steps below see all 64 lanes.
 template <typename Tin, int NV, int BLOCK>
-__device__ __forceinline__ void consume(const uint4* v, int64_t i, const RowCtx& cx, Lane& L) {
+__device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx& cx, Lane& L) {
   constexpr int VEC = Elem<Tin>::kVec;
   float z[NV * VEC];
 #pragma unroll
@@ -127,13 +153,16 @@ __device__ __forceinline__ void consume(const uint4* v, int64_t i, const RowCtx&
     L.E1 = fmaf(e1, fmaxf(x1, -kBig), L.E1);
   }
 
-  // Top-1/top-2 values. An element no larger than thr2 cannot change the
-  // row's result: some lane already holds two values >= it at lower indices
-  // (every step lies above the previous ones in index order). thr2 rises
-  // quickly, so the update below runs on few steps; it takes the step's own
-  // top two values by a pairwise tournament and merges them into the lane's.
-  // Where t1 rises, only the step is recorded; its exact index is found once
-  // the stretch is done (recover_argmax).
+  // Top-1/top-2 values. A logit cannot change the row's result if it is no
+  // larger than w2, the wave's second value so far (the wave holds two
+  // values >= it at lower indices: every step lies above the previous ones
+  // in index order), or smaller than b2, a value that some wave of the
+  // workgroup holds twice over (strictly smaller: that wave's logits may lie
+  // at higher indices). thr2 = max(w2, the float below b2) rises quickly, so
+  // the update below runs on few steps; it takes the step's own top two
+  // values by a pairwise tournament and merges them into the lane's. Where
+  // t1 rises, only the step is recorded; its exact index is found once the
+  // stretch is done.
   if (__any(cmax > L.thr2)) {
     float c1, c2;
     top2_of<NV * VEC>(z, c1, c2);  // last use of z: may reuse its registers
@@ -142,7 +171,10 @@ __device__ __forceinline__ void consume(const uint4* v, int64_t i, const RowCtx&
       L.t1 = c1;
       L.t1v = static_cast<int32_t>(i);
     }
-    L.thr2 = wave_max(L.t2);
+    float w1 = L.t1, w2 = L.t2;
+    wave_top2_values(w1, w2);
+    const float b2 = block_share_max(&scan_block().second_key, w2);
+    L.thr2 = fmaxf(w2, b2 == -INFINITY ? -INFINITY : next_below(b2));
   }
 
 }
@@ -255,16 +287,37 @@ __device__ __forceinline__ int64_t head_elems(const void* row, int32_t V) {
 
 template <typename Tin>
 __device__ RowCtx row_ctx(const RowArgs& a, int64_t r, const void* row) {
+  constexpr int VEC = Elem<Tin>::kVec;
   RowCtx cx;
   const float T = a.temperature[r];
+  cx.T = T;
   // A rejected temperature still gets a finite scale, so that the
   // non-finite-logit check does not depend on it.
   cx.c = temperature_ok(T) ? kLog2e / T : kLog2e;
   cx.h = head_elems<Tin>(row, a.V);
+  cx.fix_vec = 0;
   const int32_t y = a.sampled_ids[r];
   if (y >= 0 && y < a.V) {
     cx.y = y;
-    cx.zy = Elem<Tin>::load1(row, y);
+    const int64_t q = static_cast<int64_t>(y) - cx.h;
+    if (q >= 0 && q / VEC < (a.V - cx.h) / VEC) {
+      // y lies in an aligned vector: one 16-byte load gives z_y and the
+      // ties before y inside that vector (which the vector loop leaves out).
+      const vec4u* vp = reinterpret_cast<const vec4u*>(static_cast<const Tin*>(row) + cx.h);
+      float z[VEC];
+      Elem<Tin>::unpack(vp[q / VEC], z);
+      const int k = static_cast<int>(q % VEC);
+      float zy = z[0];
+#pragma unroll
+      for (int j = 1; j < VEC; ++j) zy = (j == k) ? z[j] : zy;
+      uint32_t f = 0;
+#pragma unroll
+      for (int j = 0; j < VEC - 1; ++j) f += (j < k && z[j] == zy) ? 1u : 0u;
+      cx.zy = zy;
+      cx.fix_vec = f;
+    } else {
+      cx.zy = Elem<Tin>::load1(row, y);
+    }
     cx.thr_before = (cx.zy == -INFINITY) ? -INFINITY : next_below(cx.zy);
     cx.thr_lo = cx.thr_before;
   } else {
@@ -277,11 +330,9 @@ __device__ RowCtx row_ctx(const RowArgs& a, int64_t r, const void* row) {
 }
 
 // Logits are read exactly once: nontemporal loads do not keep them cached.
-__device__ __forceinline__ uint4 load_stream(const uint4* p) {
+__device__ __forceinline__ vec4u load_stream(const vec4u* p) {
 #ifndef PR_CACHED_LOADS
-  typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-  const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-  return make_uint4(v.x, v.y, v.z, v.w);
+  return __builtin_nontemporal_load(p);
 #else
   return *p;
 #endif
@@ -289,47 +340,99 @@ __device__ __forceinline__ uint4 load_stream(const uint4* p) {
 
 // All-(-inf) vector: padding for lanes past the end of a stretch.
 template <typename Tin>
-__device__ __forceinline__ uint4 neg_inf_vec() {
+__device__ __forceinline__ vec4u neg_inf_vec() {
   const uint32_t w = sizeof(Tin) == 2 ? 0xff80ff80u : 0xff800000u;
-  return make_uint4(w, w, w, w);
+  return vec4u{w, w, w, w};
 }
 
-// Scan of the vector index range [vb, ve) of one row by one workgroup,
-// plus the scalar head (first) / tail (last) elements. Each lane keeps LD
-// 16-byte loads in flight and reduces them U at a time. Loop trip counts are
-// uniform across each wave: full rounds while the wave's last lane still has
-// LD vectors, then one predicated round in which lanes past the end see -inf
-// (a token of probability 0 that changes no result).
-template <typename Tin, int BLOCK, int U, int LD>
-__device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve, bool do_head, bool do_tail,
-                             int64_t nvec, const RowCtx& cx, Lane& L) {
-  static_assert(LD % U == 0, "load depth must be a multiple of the compute width");
-  constexpr int VEC = Elem<Tin>::kVec;
-  const Tin* base = static_cast<const Tin*>(row) + cx.h;
-  const uint4* vp = reinterpret_cast<const uint4*>(base);
-  const int t = threadIdx.x;
-  const int wave_first = t - static_cast<int>(__lane_id());
-  if (do_head) {
-    if (t < cx.h) consume_scalar(Elem<Tin>::load1(row, t), t, cx, L);
-    const float m = wave_max(L.mw);  // one reference for the whole wave again
-    if (m > L.mw) lane_rescale(L, m, cx.c);
-  }
-  int64_t i = vb + t;
-  int64_t i_last = vb + wave_first + (kWave - 1);  // the wave's last lane
-  for (; i_last + (LD - 1) * BLOCK < ve; i += LD * BLOCK, i_last += LD * BLOCK) {
-    uint4 v[LD];
+// Vector index of the first lane of the calling wave, as a wave-uniform
+// (scalar) value, so that loops bounded by it compile to scalar branches.
+__device__ __forceinline__ int wave_first_thread() {
+  return __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x));
+}
+
+// Whether every lane of the wave has LD vectors in [vb, ve).
+template <int BLOCK, int LD>
+__device__ __forceinline__ bool stretch_full(int64_t vb, int64_t ve) {
+  return vb + wave_first_thread() + (kWave - 1) + (LD - 1) * BLOCK < ve;
+}
+
+// The first LD vectors of a lane in the vector index range [vb, ve) of a
+// row (-inf past the end). Issued before the row's other inputs are read,
+// so that their latency overlaps.
+template <typename Tin, int BLOCK, int LD>
+__device__ __forceinline__ void stretch_prefetch(const void* row, int64_t h, int64_t vb, int64_t ve, vec4u (&v)[LD]) {
+  const vec4u* vp = reinterpret_cast<const vec4u*>(static_cast<const Tin*>(row) + h);
+  const int64_t i = vb + threadIdx.x;
+  if (stretch_full<BLOCK, LD>(vb, ve)) {
 #pragma unroll
     for (int u = 0; u < LD; ++u) v[u] = load_stream(vp + i + u * BLOCK);
-#pragma unroll
-    for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK>(v + c, i + c * BLOCK, cx, L);
-  }
-  if (i - static_cast<int64_t>(__lane_id()) < ve) {  // the wave's first lane has vectors left
-    uint4 v[LD];
+  } else {
 #pragma unroll
     for (int u = 0; u < LD; ++u) {
       const int64_t j = i + u * BLOCK;
       v[u] = j < ve ? load_stream(vp + j) : neg_inf_vec<Tin>();
     }
+  }
+}
+
+// Scan of the vector index range [vb, ve) of one row by one workgroup,
+// plus the scalar head (first) / tail (last) elements. v holds the lane's
+// first LD vectors (stretch_prefetch). Each lane keeps LD 16-byte loads in
+// flight: it reduces U vectors, then reloads their registers with the
+// vectors LD steps ahead. Loop trip counts are uniform across each wave:
+// unpredicated rounds while every reload of the round lies inside the
+// range for the whole wave, then one round whose reloads are predicated,
+// in which lanes past the end see -inf (a token of probability 0 that
+// changes no result). A wave with fewer than LD vectors in some lane holds
+// its whole share after the prefetch.
+template <typename Tin, int BLOCK, int U, int LD>
+__device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve, bool do_head, bool do_tail,
+                             int64_t nvec, const RowCtx& cx, Lane& L, vec4u (&v)[LD]) {
+  static_assert(LD % U == 0, "load depth must be a multiple of the compute width");
+  constexpr int VEC = Elem<Tin>::kVec;
+  const Tin* base = static_cast<const Tin*>(row) + cx.h;
+  const vec4u* vp = reinterpret_cast<const vec4u*>(base);
+  const int t = threadIdx.x;
+  if (t == 0) scan_block().second_key = float_key(-INFINITY);
+  __syncthreads();
+  if (do_head) {
+    if (t < cx.h) consume_scalar(Elem<Tin>::load1(row, t), t, cx, L);
+    const float m = wave_max(L.mw);  // one reference for the whole wave again
+    if (m > L.mw) lane_rescale(L, m, cx.c);
+  }
+  int64_t i = vb + t;                          // the lane's vector in v[0]
+  int64_t i0 = vb + wave_first_thread();       // the same for the wave's first lane (scalar)
+  if (stretch_full<BLOCK, LD>(vb, ve)) {
+    // Two buffers: v (carried from one round to the next) and w (local to
+    // the round). The loads of one buffer are issued before the other is
+    // reduced, so at least LD loads per lane are always in flight.
+    for (; i0 + (kWave - 1) + (3 * LD - 1) * BLOCK < ve; i += 2 * LD * BLOCK, i0 += 2 * LD * BLOCK) {
+      vec4u w[LD];
+#pragma unroll
+      for (int u = 0; u < LD; ++u) w[u] = load_stream(vp + i + (LD + u) * BLOCK);
+#pragma unroll
+      for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK>(v + c, i + c * BLOCK, cx, L);
+#pragma unroll
+      for (int u = 0; u < LD; ++u) v[u] = load_stream(vp + i + (2 * LD + u) * BLOCK);
+#pragma unroll
+      for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK>(w + c, i + (LD + c) * BLOCK, cx, L);
+    }
+    // v is inside the range; the vectors after it (fewer than 2 * LD per
+    // lane) follow in at most two predicated rounds.
+    for (; i0 < ve; i += LD * BLOCK, i0 += LD * BLOCK) {
+      vec4u w[LD];
+#pragma unroll
+      for (int u = 0; u < LD; ++u) {
+        const int64_t j = i + (LD + u) * BLOCK;
+        w[u] = j < ve ? load_stream(vp + j) : neg_inf_vec<Tin>();
+      }
+#pragma unroll
+      for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK>(v + c, i + c * BLOCK, cx, L);
+#pragma unroll
+      for (int u = 0; u < LD; ++u) v[u] = w[u];
+    }
+  } else if (i0 < ve) {
 #pragma unroll
     for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK>(v + c, i + c * BLOCK, cx, L);
   }
@@ -356,29 +459,28 @@ __device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve,
   }
 }
 
-// Rank corrections that the vector loop leaves out, summed over the block:
-// ties z == z_y before y inside y's own vector, and -- only when z_y = -inf --
-// the -inf logits of the vectors before y's vector.
+// Rank corrections that the vector loop leaves out: ties z == z_y before y
+// inside y's own vector (counted when the row context was read) and -- only
+// when z_y = -inf -- the -inf logits of the vectors before y's vector,
+// summed over the block. z_y is the same in every thread, so the barrier
+// below is reached by all threads or by none.
 template <typename Tin, int BLOCK>
 __device__ uint32_t rank_fixup(const void* row, int32_t V, int64_t nvec, const RowCtx& cx) {
   constexpr int VEC = Elem<Tin>::kVec;
-  __shared__ uint32_t sh_fix[BLOCK / kWave];
   if (cx.y < 0) return 0;
+  if (cx.zy != -INFINITY) return cx.fix_vec;
+  __shared__ uint32_t sh_fix[BLOCK / kWave];
   const int64_t vend = cx.h + nvec * VEC;
   const bool y_in_vec = cx.y >= cx.h && cx.y < vend;
   const int64_t vs = y_in_vec ? cx.h + ((cx.y - cx.h) / VEC) * VEC : 0;
+  const int64_t lim = y_in_vec ? vs : (cx.y >= vend ? vend : cx.h);
   uint32_t fix = 0;
-  if (y_in_vec && threadIdx.x < cx.y - vs)
-    fix += (Elem<Tin>::load1(row, vs + threadIdx.x) == cx.zy) ? 1u : 0u;
-  if (cx.zy == -INFINITY) {
-    const int64_t lim = y_in_vec ? vs : (cx.y >= vend ? vend : cx.h);
-    for (int64_t e = cx.h + threadIdx.x; e < lim; e += BLOCK)
-      fix += (Elem<Tin>::load1(row, e) == -INFINITY) ? 1u : 0u;
-  }
+  for (int64_t e = cx.h + threadIdx.x; e < lim; e += BLOCK)
+    fix += (Elem<Tin>::load1(row, e) == -INFINITY) ? 1u : 0u;
   fix = wave_sum_u(fix);
   if (threadIdx.x % kWave == 0) sh_fix[threadIdx.x / kWave] = fix;
   __syncthreads();
-  uint32_t tot = 0;
+  uint32_t tot = cx.fix_vec;
   for (int k = 0; k < BLOCK / kWave; ++k) tot += sh_fix[k];
   return tot;
 }
@@ -393,8 +495,7 @@ struct Nucleus {
 };
 
 // Row flags known after the first pass (everything but the id and nucleus).
-__device__ __forceinline__ uint32_t row_flags(const RowArgs& a, int64_t r, const Partial& p) {
-  const float T = a.temperature[r];
+__device__ __forceinline__ uint32_t row_flags(const RowArgs& a, int64_t r, const Partial& p, float T) {
   uint32_t flags = 0;
   if (!temperature_ok(T)) flags |= PR_FLAG_BAD_TP;
   const bool nonfinite = !(fabsf(p.S) < INFINITY) || p.m == INFINITY || p.m == -INFINITY;
@@ -412,8 +513,8 @@ __device__ __forceinline__ uint32_t row_flags(const RowArgs& a, int64_t r, const
 // Returns the confidence tuple A = (logprob, maxprob, -entropy, margin).
 __device__ void finalize_row(const RowArgs& a, int64_t r, const Partial& p, const RowCtx& cx, uint32_t fix,
                              float* conf, const Nucleus* nuc = nullptr) {
-  const float T = a.temperature[r];
-  uint32_t flags = row_flags(a, r, p);
+  const float T = cx.T;
+  uint32_t flags = row_flags(a, r, p, T);
   const float qnan = __uint_as_float(0x7fc00000u);
   float max_logit = qnan, lse = qnan, entropy = qnan, logprob = qnan, maxprob = qnan, margin = qnan;
   int32_t rank = -1, argmax = -1, cutoff = -1;
@@ -476,19 +577,48 @@ __device__ void finalize_row(const RowArgs& a, int64_t r, const Partial& p, cons
   }
 }
 
-// Streaming: the row's token joins its request slot's running state.
-__device__ void stream_update(const StreamDev& s, int32_t slot, const float* conf) {
-  if (slot < 0 || slot >= s.max_slots) return;
-  const int32_t n = s.count[slot];
+// Streaming: a request slot's running state, read when the row starts (a
+// slot appears at most once per step, so nothing else changes it meanwhile).
+struct SlotState {
+  int32_t slot;  // -1: no streaming update
+  int32_t n;
+  uint32_t nanbits;
+  double sum[4];
+  float minv[4];
+};
+
+__device__ __forceinline__ SlotState slot_load(const RowArgs& a, int64_t r) {
+  SlotState ss;
+  ss.slot = -1;
+  if (!a.slot_ids) return ss;
+  const int32_t slot = a.slot_ids[r];
+  if (slot < 0 || slot >= a.st.max_slots) return ss;
+  ss.slot = slot;
+  ss.n = a.st.count[slot];
+  ss.nanbits = a.st.nanbits[slot];
+#pragma unroll
+  for (int f = 0; f < 4; ++f) {
+    ss.sum[f] = a.st.sum[slot * 4 + f];
+    ss.minv[f] = a.st.minv[slot * 4 + f];
+  }
+  return ss;
+}
+
+// The row's token joins its request slot: count, sums and minima of the
+// non-NaN values of A, NaN bits, and the token's A in the slot's history.
+__device__ void stream_update(const StreamDev& s, const SlotState& ss, const float* conf) {
+  if (ss.slot < 0) return;
+  const int32_t slot = ss.slot;
+  const int32_t n = ss.n;
   s.count[slot] = n + 1;
-  uint32_t nanbits = s.nanbits[slot];
+  uint32_t nanbits = ss.nanbits;
   for (int f = 0; f < 4; ++f) {
     const float v = conf[f];
     if (v != v) {
       nanbits |= 1u << f;
     } else {
-      s.sum[slot * 4 + f] += static_cast<double>(v);
-      s.minv[slot * 4 + f] = fminf(s.minv[slot * 4 + f], v);
+      s.sum[slot * 4 + f] = ss.sum[f] + static_cast<double>(v);
+      s.minv[slot * 4 + f] = fminf(ss.minv[f], v);
     }
     if (n < s.max_len) s.hist[(static_cast<int64_t>(slot) * 4 + f) * s.max_len + n] = v;
   }

@@ -58,7 +58,7 @@ __device__ __forceinline__ void for_each_logit(const void* row, int32_t V, int64
   constexpr int VEC = Elem<Tin>::kVec;
   const int t = threadIdx.x;
   if (t < h) fn(Elem<Tin>::load1(row, t));
-  const uint4* vp = reinterpret_cast<const uint4*>(static_cast<const Tin*>(row) + h);
+  const vec4u* vp = reinterpret_cast<const vec4u*>(static_cast<const Tin*>(row) + h);
   for (int64_t i = t; i < nvec; i += kTpBlock) {
     float z[VEC];
     Elem<Tin>::unpack(vp[i], z);
@@ -229,20 +229,24 @@ __global__ __launch_bounds__(kTpBlock) void topp_kernel(RowArgs a) {
   if (r >= a.n_rows) return;
   constexpr int VEC = Elem<Tin>::kVec;
   const void* row = static_cast<const Tin*>(a.logits) + r * a.row_stride;
+  const int64_t h = head_elems<Tin>(row, a.V);
+  const int64_t nvec = (a.V - h) / VEC;
+  constexpr int kLD = 4;  // loads in flight per lane: 4 to 8 with double buffering
+  vec4u v[kLD];
+  stretch_prefetch<Tin, kTpBlock, kLD>(row, h, 0, nvec, v);
   const RowCtx cx = row_ctx<Tin>(a, r, row);
-  const int64_t nvec = (a.V - cx.h) / VEC;
 
   // 1. stats pass
   Lane L;
   lane_init(L);
-  scan_stretch<Tin, kTpBlock, 2, 8>(row, a.V, 0, nvec, true, true, nvec, cx, L);
+  scan_stretch<Tin, kTpBlock, 2, kLD>(row, a.V, 0, nvec, true, true, nvec, cx, L, v);
   Partial p = block_merge<kTpBlock>(L, cx.c);
   const uint32_t fix = rank_fixup<Tin, kTpBlock>(row, a.V, nvec, cx);
   if (threadIdx.x == 0) {
     sh.p = p;
     sh.fix = fix;
     const float P = a.top_p[r];
-    sh.active = (row_flags(a, r, p) & (PR_FLAG_NONFINITE | PR_FLAG_BAD_TP)) == 0 && P < 1.0f;
+    sh.active = (row_flags(a, r, p, cx.T) & (PR_FLAG_NONFINITE | PR_FLAG_BAD_TP)) == 0 && P < 1.0f;
   }
   __syncthreads();
   p = sh.p;
@@ -254,7 +258,7 @@ __global__ __launch_bounds__(kTpBlock) void topp_kernel(RowArgs a) {
     return;
   }
 
-  const float T = a.temperature[r];
+  const float T = cx.T;
   Dist D;
   D.M = p.m;
   D.invT = 1.0f / T;
