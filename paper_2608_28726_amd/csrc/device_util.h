@@ -175,28 +175,6 @@ __device__ __forceinline__ uint32_t wave_sum_u(uint32_t v) {
   return lane63(v);
 }
 
-// Largest and second value of the multiset of all lanes' (a1, a2) pairs
-// (a1 >= a2 in every lane); the result is in every lane.
-__device__ __forceinline__ void wave_top2_values(float& a1, float& a2) {
-  using namespace dpp;
-#define PR_TOP2_STEP(CTRL, MASK)                                           \
-  {                                                                        \
-    const float o1 = movf<CTRL, MASK>(-INFINITY, a1);                      \
-    const float o2 = movf<CTRL, MASK>(-INFINITY, a2);                      \
-    a2 = fmaxf(fminf(a1, o1), fmaxf(a2, o2));                              \
-    a1 = fmaxf(a1, o1);                                                    \
-  }
-  PR_TOP2_STEP(kXor1, 0xf)
-  PR_TOP2_STEP(kXor2, 0xf)
-  PR_TOP2_STEP(kHalfMirror, 0xf)
-  PR_TOP2_STEP(kMirror, 0xf)
-  PR_TOP2_STEP(kBcast15, 0xa)
-  PR_TOP2_STEP(kBcast31, 0xc)
-#undef PR_TOP2_STEP
-  a1 = lane63(a1);
-  a2 = lane63(a2);
-}
-
 // (t1, t1i, t2) merge: larger value first, equal values by lower index; the
 // second value is the larger of the loser's top-1 and both top-2 values.
 __device__ __forceinline__ void top2_merge(float& t1, int32_t& t1i, float& t2, float o1, int32_t o1i, float o2) {

@@ -57,7 +57,9 @@ void row_features_kernel(RowArgs a) {
 
   Lane L;
   lane_init(L);
-  scan_stretch<Tin, BLOCK, U, LD>(row, a.V, vb, ve, g == 0, g == G - 1, nvec, cx, L, v);
+  // Workgroups of 512 or more threads run one per CU: there the bucket of
+  // each lane's maximum is kept in registers rather than read back at the end.
+  scan_stretch<Tin, BLOCK, U, LD, (BLOCK >= 512)>(row, a.V, vb, ve, g == 0, g == G - 1, nvec, cx, L, v);
   const Partial p = block_merge<BLOCK>(L, cx.c);
   if (SPLIT) {
     if (threadIdx.x == 0) a.ws[r * G + g] = p;
@@ -131,18 +133,32 @@ constexpr int load_depth_for() {
 #ifndef PR_WIDE_BLOCK
 #define PR_WIDE_BLOCK 1024
 #endif
-// Below this many rows a row gets one wide workgroup (or several, split),
-// so that small batches need a single launch and still fill the chip.
+#ifndef PR_MID_BLOCK
+#define PR_MID_BLOCK 256
+#endif
+#ifndef PR_SPLIT_BLOCK
+#define PR_SPLIT_BLOCK 512
+#endif
+// Workgroup size by batch size: below kWideRows rows a row gets one wider
+// workgroup, so that small batches still fill the chip in a single launch:
+// kMidBlock threads while there are more rows than CUs, kWideBlock threads
+// up to one row per CU, and G workgroups of kSplitBlock threads per row
+// (merged by a second kernel) when a row per CU would leave most CUs idle.
 constexpr int64_t kWideRows = PR_WIDE_ROWS;
 constexpr int kWideBlock = PR_WIDE_BLOCK;
-constexpr int kWideTarget = 256;  // wide workgroups per launch: one per CU
+constexpr int kMidBlock = PR_MID_BLOCK;
+constexpr int kSplitBlock = PR_SPLIT_BLOCK;
+#ifndef PR_WIDE_TARGET
+#define PR_WIDE_TARGET 256
+#endif
+constexpr int kWideTarget = PR_WIDE_TARGET;  // wide workgroups per launch: one per CU
 
 int row_split(int64_t n_rows, int32_t V, pr_dtype dtype) {
   const int VEC = dtype == PR_BF16 ? 8 : 4;
   const int64_t nvec = V / VEC;
   if (n_rows <= 0 || n_rows >= kWideTarget) return 1;
   int64_t G = kWideTarget / n_rows;  // one round of at most kWideTarget workgroups
-  const int64_t by_work = nvec / (kWideBlock * 4);  // at least ~4 vectors per lane
+  const int64_t by_work = nvec / (kSplitBlock * 4);  // at least ~4 vectors per lane
   if (G > by_work) G = by_work;
   if (G > kMaxSplit) G = kMaxSplit;
   if (G < 1) G = 1;
@@ -167,10 +183,12 @@ static hipError_t launch_typed(const RowArgs& a, hipStream_t stream) {
   const dim3 grid(static_cast<unsigned>(a.n_rows * a.G));
   if (a.n_rows >= kWideRows) {
     row_features_kernel<Tin, kBlock, U, LD, false><<<grid, kBlock, 0, stream>>>(a);
+  } else if (a.n_rows > 256) {
+    row_features_kernel<Tin, kMidBlock, U, LDW, false><<<grid, kMidBlock, 0, stream>>>(a);
   } else if (a.G == 1) {
     row_features_kernel<Tin, kWideBlock, U, LDW, false><<<grid, kWideBlock, 0, stream>>>(a);
   } else {
-    row_features_kernel<Tin, kWideBlock, U, LDW, true><<<grid, kWideBlock, 0, stream>>>(a);
+    row_features_kernel<Tin, kSplitBlock, U, LDW, true><<<grid, kSplitBlock, 0, stream>>>(a);
     row_merge_kernel<Tin, kWave><<<dim3(static_cast<unsigned>(a.n_rows)), kWave, 0, stream>>>(a);
   }
   return hipGetLastError();

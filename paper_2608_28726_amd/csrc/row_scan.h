@@ -13,11 +13,11 @@ struct Lane {
   float a;         // reference of S and E: mw * c, or kNegSentinel
   float S0, S1;    // two accumulators of sum 2^x (alternating elements)
   float E0, E1;    // two accumulators of sum 2^x * x
-  float t1, t2;    // largest and second value this lane recorded
+  float t1, t2;    // largest and second largest maximum of the lane's buckets (a
+                   // step's vectors form one bucket, a scalar head/tail logit one)
   int32_t t1i;     // index of t1 (lowest among ties), once known
   int32_t t1v;     // first vector index of the step where t1 was set (-1: t1i is exact)
   uint32_t cnt;    // rank counts (ballot totals are added in lane 0 only)
-  float thr2;      // wave-uniform: max over the wave's lanes of t2
 };
 
 struct RowCtx {
@@ -31,30 +31,6 @@ struct RowCtx {
   int64_t h;         // scalar head elements before the first aligned vector
 };
 
-// A value shared by the waves of a workgroup while they scan one stretch,
-// as a sortable key updated by LDS atomic max: the largest value v such that
-// some wave holds two logits >= v (a skip threshold for the top-2 update).
-// It only decides which steps take the exact update, so results do not
-// depend on the order of the atomics; a stale read only makes a wave more
-// conservative. (The exponent sums keep per-wave references: a shared one
-// would make their rounding depend on timing.)
-struct ScanBlock {
-  uint32_t second_key;
-};
-
-__device__ __forceinline__ ScanBlock& scan_block() {
-  __shared__ ScanBlock sb;
-  return sb;
-}
-
-// Publishes v and returns the largest value published so far (v included).
-__device__ __forceinline__ float block_share_max(uint32_t* slot, float v) {
-  uint32_t old = 0;
-  if (__lane_id() == 0) old = atomicMax(slot, float_key(v));
-  old = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(old)));
-  return fmaxf(v, key_float(old));
-}
-
 __device__ __forceinline__ void lane_init(Lane& L) {
   L.mw = -INFINITY;
   L.a = kNegSentinel;
@@ -64,7 +40,6 @@ __device__ __forceinline__ void lane_init(Lane& L) {
   L.t1i = kNoIndex;
   L.t1v = -1;
   L.cnt = 0;
-  L.thr2 = -INFINITY;
 }
 
 // Moves the lane's reference up to a_new = m_new * c (m_new >= the old max).
@@ -81,35 +56,13 @@ __device__ __forceinline__ void lane_rescale(Lane& L, float m_new, float c) {
   L.a = a_new;
 }
 
-// Largest and second largest of N values (duplicates count), by a pairwise
-// tournament: leaves keep (max, min) of pairs, merges keep
-// (max of maxima, max of the smaller maximum and both seconds).
-template <int N>
-__device__ __forceinline__ void top2_of(const float* z, float& c1, float& c2) {
-  float h[N / 2], s2[N / 2];
-#pragma unroll
-  for (int k = 0; k < N / 2; ++k) {
-    h[k] = fmaxf(z[2 * k], z[2 * k + 1]);
-    s2[k] = fminf(z[2 * k], z[2 * k + 1]);
-  }
-#pragma unroll
-  for (int w = N / 2; w > 1; w >>= 1) {
-#pragma unroll
-    for (int k = 0; k < w / 2; ++k) {
-      const float a = h[2 * k], b = h[2 * k + 1];
-      s2[k] = fmaxf(fminf(a, b), fmaxf(s2[2 * k], s2[2 * k + 1]));
-      h[k] = fmaxf(a, b);
-    }
-  }
-  c1 = h[0];
-  c2 = s2[0];
-}
-
 // NV vectors of one lane; vector u has vector index i + u * BLOCK. Every lane
 // of the wave calls this together (wave-uniform control flow), so the
-// cross-lane steps below see all 64 lanes.
-template <typename Tin, int NV, int BLOCK>
-__device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx& cx, Lane& L) {
+// cross-lane steps below see all 64 lanes. With KEEP, keep[] receives the
+// step's vectors whenever they raise the lane's t1 (the bucket is then read
+// from registers, not memory, once the stretch is done).
+template <typename Tin, int NV, int BLOCK, bool KEEP>
+__device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx& cx, Lane& L, vec4u* keep) {
   constexpr int VEC = Elem<Tin>::kVec;
   float z[NV * VEC];
 #pragma unroll
@@ -122,21 +75,6 @@ __device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx&
   // The wave shares one reference, its running maximum: every exponent
   // argument stays <= 0 and the reference moves only on a new wave maximum.
   if (__any(cmax > L.mw)) lane_rescale(L, wave_max(cmax), cx.c);
-
-  // Rank of y: a vector wholly before y counts z >= z_y (z > next_below(z_y)),
-  // any other vector counts z > z_y; ties before y inside y's own vector are
-  // added once when the row is finalised. Ballot totals are wave-wide.
-  if (__any(cmax > cx.thr_lo)) {
-    uint32_t c = 0;
-#pragma unroll
-    for (int u = 0; u < NV; ++u) {
-      const int64_t last = cx.h + (i + u * BLOCK) * VEC + (VEC - 1);
-      const float thr = (last < cx.y) ? cx.thr_before : cx.zy;
-#pragma unroll
-      for (int k = 0; k < VEC; ++k) c += __popcll(__ballot(z[u * VEC + k] > thr));
-    }
-    if (__lane_id() == 0) L.cnt += c;
-  }
 
   // Sum of 2^x and of 2^x * x. A masked logit (-inf) has x = -inf and
   // 2^x = 0; x is clamped to a finite value so that 0 * x stays 0.
@@ -153,30 +91,35 @@ __device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx&
     L.E1 = fmaf(e1, fmaxf(x1, -kBig), L.E1);
   }
 
-  // Top-1/top-2 values. A logit cannot change the row's result if it is no
-  // larger than w2, the wave's second value so far (the wave holds two
-  // values >= it at lower indices: every step lies above the previous ones
-  // in index order), or smaller than b2, a value that some wave of the
-  // workgroup holds twice over (strictly smaller: that wave's logits may lie
-  // at higher indices). thr2 = max(w2, the float below b2) rises quickly, so
-  // the update below runs on few steps; it takes the step's own top two
-  // values by a pairwise tournament and merges them into the lane's. Where
-  // t1 rises, only the step is recorded; its exact index is found once the
-  // stretch is done.
-  if (__any(cmax > L.thr2)) {
-    float c1, c2;
-    top2_of<NV * VEC>(z, c1, c2);  // last use of z: may reuse its registers
-    L.t2 = fmaxf(fmaxf(L.t2, c2), fminf(L.t1, c1));
-    if (c1 > L.t1) {
-      L.t1 = c1;
-      L.t1v = static_cast<int32_t>(i);
+  // Rank of y: a vector wholly before y counts z >= z_y (z > next_below(z_y)),
+  // any other vector counts z > z_y; ties before y inside y's own vector are
+  // added once when the row is finalised. Ballot totals are wave-wide. (After
+  // the sums, so that the first step need not wait for z_y.)
+  if (__any(cmax > cx.thr_lo)) {
+    uint32_t c = 0;
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      const int64_t last = cx.h + (i + u * BLOCK) * VEC + (VEC - 1);
+      const float thr = (last < cx.y) ? cx.thr_before : cx.zy;
+#pragma unroll
+      for (int k = 0; k < VEC; ++k) c += __popcll(__ballot(z[u * VEC + k] > thr));
     }
-    float w1 = L.t1, w2 = L.t2;
-    wave_top2_values(w1, w2);
-    const float b2 = block_share_max(&scan_block().second_key, w2);
-    L.thr2 = fmaxf(w2, b2 == -INFINITY ? -INFINITY : next_below(b2));
+    if (__lane_id() == 0) L.cnt += c;
   }
 
+  // Top-1/top-2 values, per bucket: the lane keeps the largest and second
+  // largest bucket maxima and the step where the largest first appeared.
+  // The second value of the stretch is the larger of the second largest
+  // bucket maximum and the second value inside the bucket of the maximum,
+  // which is examined once the stretch is done (scan_stretch).
+  const bool up = cmax > L.t1;
+  L.t2 = __builtin_amdgcn_fmed3f(L.t1, L.t2, cmax);
+  L.t1v = up ? static_cast<int32_t>(i) : L.t1v;
+  L.t1 = fmaxf(L.t1, cmax);
+  if (KEEP) {
+#pragma unroll
+    for (int u = 0; u < NV; ++u) keep[u] = up ? v[u] : keep[u];
+  }
 }
 
 // One element outside the aligned vectors (row head or tail), per lane.
@@ -197,58 +140,57 @@ __device__ __forceinline__ void consume_scalar(float z, int64_t idx, const RowCt
   L.E0 = fmaf(e, fmaxf(x, -kBig), L.E0);
 }
 
-// Block-wide merge of the lanes into one Partial (valid in thread 0).
+// Block-wide merge of the lanes into one Partial (valid in thread 0). Each
+// wave reduces its lanes to a state relative to its own largest logit and
+// publishes it; after one barrier the first wave merges the NW wave states
+// with lane-parallel reductions.
 template <int BLOCK>
 __device__ Partial block_merge(Lane& L, float c) {
   constexpr int NW = BLOCK / kWave;
-  __shared__ float sh_m[NW], sh_S[NW], sh_E[NW], sh_t1[NW], sh_t2[NW];
-  __shared__ int32_t sh_t1i[NW];
-  __shared__ uint32_t sh_cnt[NW];
+  static_assert(NW >= 1 && NW <= kWave, "one wave merges the wave states");
+  __shared__ Partial sh[NW];
   const int lane = threadIdx.x % kWave;
   const int w = threadIdx.x / kWave;
 
-  const float mw = wave_max(L.t1);
-  const uint32_t cw = wave_sum_u(L.cnt);
-  float t1 = L.t1, t2 = L.t2;
-  int32_t t1i = L.t1i;
-  wave_top2(t1, t1i, t2);
-  if (lane == 0) {
-    sh_m[w] = mw;
-    sh_t1[w] = t1;
-    sh_t1i[w] = t1i;
-    sh_t2[w] = t2;
-    sh_cnt[w] = cw;
-  }
-  __syncthreads();
-  float M = sh_m[0];
-#pragma unroll
-  for (int k = 1; k < NW; ++k) M = fmaxf(M, sh_m[k]);
-  const float A = M * c;
+  Partial q;
+  q.m = wave_max(L.t1);
   float S = L.S0 + L.S1, E = L.E0 + L.E1;
-  rebase(L.a == kNegSentinel, L.a, A, S, E);
-  S = wave_sum(S);
-  E = wave_sum(E);
-  if (lane == 0) {
-    sh_S[w] = S;
-    sh_E[w] = E;
-  }
+  rebase(L.a == kNegSentinel, L.a, q.m * c, S, E);
+  q.S = wave_sum(S);
+  q.E = wave_sum(E);
+  q.t1 = L.t1;
+  q.t1i = L.t1i;
+  q.t2 = L.t2;
+  wave_top2(q.t1, q.t1i, q.t2);
+  q.cnt = wave_sum_u(L.cnt);
+  q.pad = 0;
+  if (NW == 1) return q;
+  if (lane == 0) sh[w] = q;
   __syncthreads();
-  Partial p;
-  p.m = M;
-  p.S = 0.0f;
-  p.E = 0.0f;
-  p.t1 = -INFINITY;
-  p.t1i = kNoIndex;
-  p.t2 = -INFINITY;
-  p.cnt = 0;
-  p.pad = 0;
-  if (threadIdx.x == 0) {
-    for (int k = 0; k < NW; ++k) {
-      p.S += sh_S[k];
-      p.E += sh_E[k];
-      top2_merge(p.t1, p.t1i, p.t2, sh_t1[k], sh_t1i[k], sh_t2[k]);
-      p.cnt += sh_cnt[k];
+  Partial p = q;
+  if (w == 0) {
+    Partial e;
+    if (lane < NW) {
+      e = sh[lane];
+    } else {
+      e.m = -INFINITY;
+      e.S = 0.0f;
+      e.E = 0.0f;
+      e.t1 = -INFINITY;
+      e.t1i = kNoIndex;
+      e.t2 = -INFINITY;
+      e.cnt = 0;
+      e.pad = 0;
     }
+    p.m = wave_max(e.m);
+    rebase(e.m == -INFINITY, e.m * c, p.m * c, e.S, e.E);
+    p.S = wave_sum(e.S);
+    p.E = wave_sum(e.E);
+    wave_top2(e.t1, e.t1i, e.t2);
+    p.t1 = e.t1;
+    p.t1i = e.t1i;
+    p.t2 = e.t2;
+    p.cnt = wave_sum_u(e.cnt);
   }
   return p;
 }
@@ -386,7 +328,7 @@ __device__ __forceinline__ void stretch_prefetch(const void* row, int64_t h, int
 // in which lanes past the end see -inf (a token of probability 0 that
 // changes no result). A wave with fewer than LD vectors in some lane holds
 // its whole share after the prefetch.
-template <typename Tin, int BLOCK, int U, int LD>
+template <typename Tin, int BLOCK, int U, int LD, bool KEEP = false>
 __device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve, bool do_head, bool do_tail,
                              int64_t nvec, const RowCtx& cx, Lane& L, vec4u (&v)[LD]) {
   static_assert(LD % U == 0, "load depth must be a multiple of the compute width");
@@ -394,8 +336,11 @@ __device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve,
   const Tin* base = static_cast<const Tin*>(row) + cx.h;
   const vec4u* vp = reinterpret_cast<const vec4u*>(base);
   const int t = threadIdx.x;
-  if (t == 0) scan_block().second_key = float_key(-INFINITY);
-  __syncthreads();
+  vec4u keep[U];
+  if (KEEP) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) keep[u] = neg_inf_vec<Tin>();
+  }
   if (do_head) {
     if (t < cx.h) consume_scalar(Elem<Tin>::load1(row, t), t, cx, L);
     const float m = wave_max(L.mw);  // one reference for the whole wave again
@@ -412,11 +357,11 @@ __device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve,
 #pragma unroll
       for (int u = 0; u < LD; ++u) w[u] = load_stream(vp + i + (LD + u) * BLOCK);
 #pragma unroll
-      for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK>(v + c, i + c * BLOCK, cx, L);
+      for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK, KEEP>(v + c, i + c * BLOCK, cx, L, keep);
 #pragma unroll
       for (int u = 0; u < LD; ++u) v[u] = load_stream(vp + i + (2 * LD + u) * BLOCK);
 #pragma unroll
-      for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK>(w + c, i + (LD + c) * BLOCK, cx, L);
+      for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK, KEEP>(w + c, i + (LD + c) * BLOCK, cx, L, keep);
     }
     // v is inside the range; the vectors after it (fewer than 2 * LD per
     // lane) follow in at most two predicated rounds.
@@ -428,34 +373,44 @@ __device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve,
         w[u] = j < ve ? load_stream(vp + j) : neg_inf_vec<Tin>();
       }
 #pragma unroll
-      for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK>(v + c, i + c * BLOCK, cx, L);
+      for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK, KEEP>(v + c, i + c * BLOCK, cx, L, keep);
 #pragma unroll
       for (int u = 0; u < LD; ++u) v[u] = w[u];
     }
   } else if (i0 < ve) {
 #pragma unroll
-    for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK>(v + c, i + c * BLOCK, cx, L);
+    for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK, KEEP>(v + c, i + c * BLOCK, cx, L, keep);
   }
   if (do_tail) {
     const int64_t tail0 = cx.h + nvec * VEC;
     for (int64_t e = tail0 + t; e < V; e += BLOCK) consume_scalar(Elem<Tin>::load1(row, e), e, cx, L);
   }
-  // Exact index of the wave maximum: the lanes holding it re-read the step
-  // where their t1 was set and take its first occurrence (a few bytes per
-  // wave; ties across lanes and waves resolve by index in the merges).
+  // The lanes holding the wave maximum examine the bucket where their t1 was
+  // set (kept in registers, or re-read: a few bytes per wave): its first
+  // occurrence gives the exact index (ties across lanes and waves resolve by
+  // index in the merges), and its other logits the second value inside it.
   const float mw = wave_max(L.t1);
   if (L.t1 == mw && L.t1v >= 0) {
     int32_t best = kNoIndex;
-    for (int u = U - 1; u >= 0; --u) {
+    uint32_t n_max = 0;
+    float below = -INFINITY;
+    for (int u = 0; u < U; ++u) {
       const int64_t j = static_cast<int64_t>(L.t1v) + u * BLOCK;
-      if (j >= ve) continue;
+      if (j >= ve) break;
       float z[VEC];
-      Elem<Tin>::unpack(vp[j], z);
+      Elem<Tin>::unpack(KEEP ? keep[u] : vp[j], z);
 #pragma unroll
-      for (int k = VEC - 1; k >= 0; --k)
-        if (z[k] == mw) best = static_cast<int32_t>(cx.h + j * VEC + k);
+      for (int k = 0; k < VEC; ++k) {
+        if (z[k] == mw) {
+          if (n_max == 0) best = static_cast<int32_t>(cx.h + j * VEC + k);
+          ++n_max;
+        } else {
+          below = fmaxf(below, z[k]);
+        }
+      }
     }
     L.t1i = best;
+    L.t2 = fmaxf(L.t2, n_max >= 2 ? mw : below);
   }
 }
 
