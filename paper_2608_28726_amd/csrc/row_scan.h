@@ -56,13 +56,23 @@ __device__ __forceinline__ void lane_rescale(Lane& L, float m_new, float c) {
   L.a = a_new;
 }
 
+// Per-element hook of the scan: called once per step with the step's logits
+// z and their 2^x (relative to the lane reference L.a, after any rescale),
+// and once per scalar head/tail logit. The row kernel uses none.
+struct NoHook {
+  template <int N>
+  __device__ __forceinline__ void step(const float (&)[N], const float (&)[N], float, const Lane&) {}
+  __device__ __forceinline__ void scalar(float, float, const Lane&) {}
+};
+
 // NV vectors of one lane; vector u has vector index i + u * BLOCK. Every lane
 // of the wave calls this together (wave-uniform control flow), so the
 // cross-lane steps below see all 64 lanes. With KEEP, keep[] receives the
 // step's vectors whenever they raise the lane's t1 (the bucket is then read
 // from registers, not memory, once the stretch is done).
-template <typename Tin, int NV, int BLOCK, bool KEEP>
-__device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx& cx, Lane& L, vec4u* keep) {
+template <typename Tin, int NV, int BLOCK, bool KEEP, typename Hook = NoHook>
+__device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx& cx, Lane& L, vec4u* keep,
+                                        Hook& hook) {
   constexpr int VEC = Elem<Tin>::kVec;
   float z[NV * VEC];
 #pragma unroll
@@ -79,17 +89,21 @@ __device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx&
   // Sum of 2^x and of 2^x * x. A masked logit (-inf) has x = -inf and
   // 2^x = 0; x is clamped to a finite value so that 0 * x stays 0.
   const float na = -L.a;
+  float ev[NV * VEC];
 #pragma unroll
   for (int k = 0; k < NV * VEC; k += 2) {
     const float x0 = fmaf(z[k], cx.c, na);
     const float x1 = fmaf(z[k + 1], cx.c, na);
     const float e0 = fast_exp2(x0);
     const float e1 = fast_exp2(x1);
+    ev[k] = e0;
+    ev[k + 1] = e1;
     L.S0 += e0;
     L.S1 += e1;
     L.E0 = fmaf(e0, fmaxf(x0, -kBig), L.E0);
     L.E1 = fmaf(e1, fmaxf(x1, -kBig), L.E1);
   }
+  hook.step(z, ev, cmax, L);
 
   // Rank of y: a vector wholly before y counts z >= z_y (z > next_below(z_y)),
   // any other vector counts z > z_y; ties before y inside y's own vector are
@@ -123,7 +137,8 @@ __device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx&
 }
 
 // One element outside the aligned vectors (row head or tail), per lane.
-__device__ __forceinline__ void consume_scalar(float z, int64_t idx, const RowCtx& cx, Lane& L) {
+template <typename Hook = NoHook>
+__device__ __forceinline__ void consume_scalar(float z, int64_t idx, const RowCtx& cx, Lane& L, Hook& hook) {
   if (z > L.mw) lane_rescale(L, z, cx.c);
   if (z > L.t1) {
     L.t2 = L.t1;
@@ -138,6 +153,7 @@ __device__ __forceinline__ void consume_scalar(float z, int64_t idx, const RowCt
   const float e = fast_exp2(x);
   L.S0 += e;
   L.E0 = fmaf(e, fmaxf(x, -kBig), L.E0);
+  hook.scalar(z, e, L);
 }
 
 // Block-wide merge of the lanes into one Partial (valid in thread 0). Each
@@ -318,50 +334,34 @@ __device__ __forceinline__ void stretch_prefetch(const void* row, int64_t h, int
   }
 }
 
-// Scan of the vector index range [vb, ve) of one row by one workgroup,
-// plus the scalar head (first) / tail (last) elements. v holds the lane's
-// first LD vectors (stretch_prefetch). Each lane keeps LD 16-byte loads in
-// flight: it reduces U vectors, then reloads their registers with the
-// vectors LD steps ahead. Loop trip counts are uniform across each wave:
-// unpredicated rounds while every reload of the round lies inside the
-// range for the whole wave, then one round whose reloads are predicated,
-// in which lanes past the end see -inf (a token of probability 0 that
-// changes no result). A wave with fewer than LD vectors in some lane holds
-// its whole share after the prefetch.
-template <typename Tin, int BLOCK, int U, int LD, bool KEEP = false>
-__device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve, bool do_head, bool do_tail,
-                             int64_t nvec, const RowCtx& cx, Lane& L, vec4u (&v)[LD]) {
+// The loop over the vector index range [vb, ve) of a row shared by every
+// pass: v holds the lane's first LD vectors (stretch_prefetch); body(vv, j)
+// reduces the U vectors vv[0..U) of indices j + u * BLOCK. Each lane keeps LD
+// 16-byte loads in flight with two buffers: v (carried from one round to
+// the next) and w (local to the round); the loads of one are issued before
+// the other is reduced, so at least LD loads per lane are in flight. Loop
+// trip counts are uniform across each wave: unpredicated rounds while every
+// load of the round lies inside the range for the whole wave, then rounds
+// whose loads are predicated, in which lanes past the end see -inf (a token
+// of probability 0 that changes no result). A wave with fewer than LD
+// vectors in some lane holds its whole share after the prefetch. Steps of a
+// wave are reduced in increasing index order.
+template <typename Tin, int BLOCK, int U, int LD, typename Body>
+__device__ __forceinline__ void stream_stretch(const vec4u* vp, int64_t vb, int64_t ve, vec4u (&v)[LD], Body&& body) {
   static_assert(LD % U == 0, "load depth must be a multiple of the compute width");
-  constexpr int VEC = Elem<Tin>::kVec;
-  const Tin* base = static_cast<const Tin*>(row) + cx.h;
-  const vec4u* vp = reinterpret_cast<const vec4u*>(base);
-  const int t = threadIdx.x;
-  vec4u keep[U];
-  if (KEEP) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) keep[u] = neg_inf_vec<Tin>();
-  }
-  if (do_head) {
-    if (t < cx.h) consume_scalar(Elem<Tin>::load1(row, t), t, cx, L);
-    const float m = wave_max(L.mw);  // one reference for the whole wave again
-    if (m > L.mw) lane_rescale(L, m, cx.c);
-  }
-  int64_t i = vb + t;                          // the lane's vector in v[0]
-  int64_t i0 = vb + wave_first_thread();       // the same for the wave's first lane (scalar)
+  int64_t i = vb + threadIdx.x;                 // the lane's vector in v[0]
+  int64_t i0 = vb + wave_first_thread();        // the same for the wave's first lane (scalar)
   if (stretch_full<BLOCK, LD>(vb, ve)) {
-    // Two buffers: v (carried from one round to the next) and w (local to
-    // the round). The loads of one buffer are issued before the other is
-    // reduced, so at least LD loads per lane are always in flight.
     for (; i0 + (kWave - 1) + (3 * LD - 1) * BLOCK < ve; i += 2 * LD * BLOCK, i0 += 2 * LD * BLOCK) {
       vec4u w[LD];
 #pragma unroll
       for (int u = 0; u < LD; ++u) w[u] = load_stream(vp + i + (LD + u) * BLOCK);
 #pragma unroll
-      for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK, KEEP>(v + c, i + c * BLOCK, cx, L, keep);
+      for (int c = 0; c < LD; c += U) body(v + c, i + c * BLOCK);
 #pragma unroll
       for (int u = 0; u < LD; ++u) v[u] = load_stream(vp + i + (2 * LD + u) * BLOCK);
 #pragma unroll
-      for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK, KEEP>(w + c, i + (LD + c) * BLOCK, cx, L, keep);
+      for (int c = 0; c < LD; c += U) body(w + c, i + (LD + c) * BLOCK);
     }
     // v is inside the range; the vectors after it (fewer than 2 * LD per
     // lane) follow in at most two predicated rounds.
@@ -373,17 +373,42 @@ __device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve,
         w[u] = j < ve ? load_stream(vp + j) : neg_inf_vec<Tin>();
       }
 #pragma unroll
-      for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK, KEEP>(v + c, i + c * BLOCK, cx, L, keep);
+      for (int c = 0; c < LD; c += U) body(v + c, i + c * BLOCK);
 #pragma unroll
       for (int u = 0; u < LD; ++u) v[u] = w[u];
     }
   } else if (i0 < ve) {
 #pragma unroll
-    for (int c = 0; c < LD; c += U) consume<Tin, U, BLOCK, KEEP>(v + c, i + c * BLOCK, cx, L, keep);
+    for (int c = 0; c < LD; c += U) body(v + c, i + c * BLOCK);
   }
+}
+
+// Scan of the vector index range [vb, ve) of one row by one workgroup,
+// plus the scalar head (first) / tail (last) elements (stream_stretch does
+// the vectors; v holds the lane's first LD vectors).
+template <typename Tin, int BLOCK, int U, int LD, bool KEEP = false, typename Hook = NoHook>
+__device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve, bool do_head, bool do_tail,
+                             int64_t nvec, const RowCtx& cx, Lane& L, vec4u (&v)[LD], Hook&& hook = Hook()) {
+  constexpr int VEC = Elem<Tin>::kVec;
+  const Tin* base = static_cast<const Tin*>(row) + cx.h;
+  const vec4u* vp = reinterpret_cast<const vec4u*>(base);
+  const int t = threadIdx.x;
+  vec4u keep[U];
+  if (KEEP) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) keep[u] = neg_inf_vec<Tin>();
+  }
+  if (do_head) {
+    if (t < cx.h) consume_scalar(Elem<Tin>::load1(row, t), t, cx, L, hook);
+    const float m = wave_max(L.mw);  // one reference for the whole wave again
+    if (m > L.mw) lane_rescale(L, m, cx.c);
+  }
+  stream_stretch<Tin, BLOCK, U, LD>(vp, vb, ve, v, [&](const vec4u* vv, int64_t j) {
+    consume<Tin, U, BLOCK, KEEP>(vv, j, cx, L, keep, hook);
+  });
   if (do_tail) {
     const int64_t tail0 = cx.h + nvec * VEC;
-    for (int64_t e = tail0 + t; e < V; e += BLOCK) consume_scalar(Elem<Tin>::load1(row, e), e, cx, L);
+    for (int64_t e = tail0 + t; e < V; e += BLOCK) consume_scalar(Elem<Tin>::load1(row, e), e, cx, L, hook);
   }
   // The lanes holding the wave maximum examine the bucket where their t1 was
   // set (kept in registers, or re-read: a few bytes per wave): its first

@@ -4,21 +4,34 @@
 // features are then those of the renormalised nucleus (the per-token
 // features of Pro-Router, Sec. 3.1, Eq. 3, after top-p truncation).
 //
-// One 512-thread workgroup per row, at most five reads of the row:
-//  1. the stats pass of the row kernel (max M, rank of y, argmax, margin);
-//  2. a 4096-bin histogram over the distance (M - z) / T in nats of every
-//     logit within 50 nats of M, with float64 masses exp((z - M) / T) and
-//     counts in LDS, plus the float64 total S; its prefix sums give the
-//     bins [b_lo, b_hi] in which the cumulative mass crosses P * S;
-//  3. float64 sums over the bins above b_lo (mass, count, entropy term) and
-//     the logits of the crossing bins gathered into LDS;
-//  4. a bitonic sort of the gathered logits (descending) and a float64 scan
-//     along it gives the exact k. Logits beyond 50 nats can never be in a
-//     nucleus with P < 1 (their total mass is below V * e^-50 of S).
-// When the crossing bins hold more than 4096 logits, a byte-wise radix
-// refinement over order-preserving keys (four more reads) finds the boundary
-// value instead; equal logits have equal mass, so ties are resolved by
-// counting.
+// One 512-thread workgroup per row, two reads of the row in the common case:
+//  1. the stats pass of the row kernel (max M, rank of y, argmax, margin)
+//     also builds a histogram in LDS: 4096 bins over the distance
+//     (A0 - z) / T in [-25, 50) nats from an anchor A0, the workgroup's
+//     largest logit among the first vectors (known before the pass
+//     starts), each holding the count and the summed offsets of its logits
+//     from the bin centre (fixed point), plus a list of the few logits more
+//     than 25 nats above A0. A bin's mass is its count times the mass at
+//     its centre, corrected to first order by the offsets (relative error
+//     below 5e-5: bins are 0.018 nats wide); the prefix sums locate a window
+//     of bins whose cumulative mass brackets P of the total with a relative
+//     margin of 5e-4. (Integer LDS atomics are far cheaper than float ones);
+//  2. an exact pass: float64 sums of mass, count and entropy term over the
+//     logits above the window, the window's logits gathered into LDS, and
+//     the float64 total over every logit within 50 nats of M;
+//  3. a bitonic sort of the window (descending) and a float64 scan along it
+//     give the exact k; the crossing is verified to lie inside the window.
+// Logits beyond 50 nats can never be in a nucleus with P < 1 (their total
+// mass is below V * e^-50 of S). Float64 exponentials use a table-driven
+// method (Tang, ACM TOMS 15(2), 1989): exp(d) = 2^(n/64) * exp(r) with
+// |r| <= ln2/128 and a degree-5 polynomial.
+//
+// When the histogram cannot be used (no finite anchor, an overfull list or
+// window, or a crossing outside the window) the row falls back to the
+// three-pass method: a 4096-bin float64 histogram relative to M, exact sums
+// above the crossing bins with their logits gathered, sorted and scanned,
+// and for overfull crossing bins a byte-wise radix refinement over
+// order-preserving keys (four more reads) that resolves ties by counting.
 #include "topp.h"
 
 #include "row_scan.h"
@@ -30,19 +43,39 @@ using namespace scan;
 namespace {
 
 constexpr int kTpBlock = 512;
-constexpr int kBins = 4096;
+constexpr int kBins = 4096;     // fallback histogram: bins over kDMax nats below M
 constexpr float kDMax = 50.0f;  // nats below the maximum
 constexpr int kCap = 4096;      // gathered logits sorted in LDS
 constexpr int kNW = kTpBlock / kWave;
+constexpr int kHB = 4096;         // histogram bins of the stats pass
+constexpr float kHAbove = 25.0f;  // nats above the anchor covered by the bins
+constexpr float kHSpan = 75.0f;   // nats covered: [-kHAbove, kDMax)
+constexpr float kHK = kHB / kHSpan;  // bins per nat
+constexpr int kAboveCap = 512;    // logits above the bins, kept in a list
+constexpr double kWinMargin = 5e-4;  // relative margin of the window around P * S
+constexpr float kOffQ = 4096.0f;     // fixed-point scale of the offsets from the bin centre
 
 struct TpShared {
-  double mass[kBins];
-  uint32_t cnt[kBins];
+  union {
+    struct {
+      double mass[kBins];
+      uint32_t cnt[kBins];
+    } lg;              // fallback histogram
+    struct {
+      uint32_t cnt[kHB + kWave];  // stats-pass histogram (+ one discard slot per lane)
+      int32_t off[kHB + kWave];   // summed offsets from the bin centre, times kOffQ
+    } hs;
+    double wtab[kHB];  // exact pass: exp of each bin centre's distance from M
+  } u;
   float win[kCap];
+  float above[kAboveCap];
+  double exptab[64];  // 2^(j/64)
   double red_d[2][kNW];
   uint32_t red_u[kNW];
+  float red_f[kNW];
   double S64, target, massAbove, Eabove, SN, EN;
-  uint32_t b_lo, b_hi, wcount, cntAbove, jfirst, rcount;
+  uint32_t b_lo, b_hi, wcount, cntAbove, jfirst, rcount, n_above;
+  int32_t hb_lo, hb_hi;
   int32_t active;
   Partial p;
   uint32_t fix;
@@ -52,19 +85,27 @@ struct TpShared {
   uint32_t prefix, rdigit;
 };
 
-// Calls fn(z) for every logit of the row (order irrelevant).
+// Calls fn(z) for every logit of the row (order irrelevant), with the
+// double-buffered loop of the scan (lanes past the end see -inf, which every
+// fn ignores).
 template <typename Tin, typename Fn>
 __device__ __forceinline__ void for_each_logit(const void* row, int32_t V, int64_t h, int64_t nvec, Fn fn) {
   constexpr int VEC = Elem<Tin>::kVec;
+  constexpr int LDX = 2, UX = 1;
   const int t = threadIdx.x;
   if (t < h) fn(Elem<Tin>::load1(row, t));
   const vec4u* vp = reinterpret_cast<const vec4u*>(static_cast<const Tin*>(row) + h);
-  for (int64_t i = t; i < nvec; i += kTpBlock) {
-    float z[VEC];
-    Elem<Tin>::unpack(vp[i], z);
+  vec4u v[LDX];
+  stretch_prefetch<Tin, kTpBlock, LDX>(row, h, 0, nvec, v);
+  stream_stretch<Tin, kTpBlock, UX, LDX>(vp, 0, nvec, v, [&](const vec4u* vv, int64_t) {
 #pragma unroll
-    for (int k = 0; k < VEC; ++k) fn(z[k]);
-  }
+    for (int u = 0; u < UX; ++u) {
+      float z[VEC];
+      Elem<Tin>::unpack(vv[u], z);
+#pragma unroll
+      for (int k = 0; k < VEC; ++k) fn(z[k]);
+    }
+  });
   for (int64_t e = h + nvec * VEC + t; e < V; e += kTpBlock) fn(Elem<Tin>::load1(row, e));
 }
 
@@ -128,6 +169,75 @@ struct Dist {
   }
   __device__ __forceinline__ double d64(float z) const {
     return (static_cast<double>(z) - static_cast<double>(M)) * invT64;
+  }
+};
+
+// exp(d) for finite d in [-700, 0] (table-driven, Tang 1989): n = round(64 d
+// / ln2) by adding and subtracting 1.5 * 2^52 (the low word of the sum is n),
+// r = d - n ln2/64 in two parts (n * kLn2By64Hi is exact for |n| < 2^24),
+// exp(r) by its degree-5 Taylor polynomial (|r| <= ln2/128: truncation below
+// 4e-17), times 2^((n mod 64) / 64) from the table, times 2^(n div 64) built
+// from its exponent bits.
+__device__ __forceinline__ double exp_tang(double d, const double* tab) {
+  constexpr double kInvLn2By64 = 0x1.71547652b82fep+6;  // 64 / ln2
+  constexpr double kLn2By64Hi = 0x1.62e42fe000000p-7;
+  constexpr double kLn2By64Lo = 0x1.f473de6af278fp-36;
+  constexpr double kShift = 0x1.8p52;
+  const double t = fma(d, kInvLn2By64, kShift);
+  const int ni = static_cast<int>(static_cast<uint32_t>(__double_as_longlong(t)));
+  const double n = t - kShift;
+  double r = fma(-n, kLn2By64Hi, d);
+  r = fma(-n, kLn2By64Lo, r);
+  double p = fma(r, 1.0 / 120.0, 1.0 / 24.0);
+  p = fma(p, r, 1.0 / 6.0);
+  p = fma(p, r, 0.5);
+  p = fma(p, r, 1.0);
+  p = fma(p, r, 1.0);
+  const double scale = __longlong_as_double(static_cast<long long>(static_cast<uint64_t>((ni >> 6) + 1023) << 52));
+  return tab[ni & 63] * p * scale;
+}
+
+// Stats-pass histogram: logit z counts in bin floor(bf), bf = fma(z, kz, k0)
+// = (A0 - z) / T * kHK + kHAbove * kHK, and adds its offset bf - floor(bf) -
+// 1/2 from the centre; bf < 0 (more than kHAbove nats above A0) goes to the
+// list instead, bf >= kHB is beyond the window. Lanes with no bin update a
+// discard slot of their own, so the update is branch-free and discards do
+// not collide. The exact pass recomputes bf with the same operands, so both
+// passes bin identically.
+struct HistHook {
+  uint32_t* cnt;
+  int32_t* off;
+  float* above;
+  uint32_t* n_above;
+  float kz, k0;  // bin coordinate
+  __device__ __forceinline__ void count(float z) {
+    const float bf = fmaf(z, kz, k0);
+    const bool in = bf >= 0.0f && bf < static_cast<float>(kHB);
+    const float bc = fminf(fmaxf(bf, 0.0f), static_cast<float>(kHB));  // NaN -> 0
+    const int b = static_cast<int>(bc);
+    const int idx = in ? b : kHB + static_cast<int>(__lane_id());
+    const float delta = bc - static_cast<float>(b) - 0.5f;  // in [-1/2, 1/2) for a counted logit
+    atomicAdd(&cnt[idx], 1u);
+    atomicAdd(&off[idx], static_cast<int32_t>(delta * kOffQ));
+  }
+  template <int N>
+  __device__ __forceinline__ void step(const float (&z)[N], const float (&)[N], float cmax, const Lane&) {
+#pragma unroll
+    for (int k = 0; k < N; ++k) count(z[k]);
+    if (__any(fmaf(cmax, kz, k0) < 0.0f)) {  // bf is non-increasing in z
+#pragma unroll
+      for (int k = 0; k < N; ++k) add_above(z[k]);
+    }
+  }
+  __device__ __forceinline__ void scalar(float z, float, const Lane&) {
+    count(z);
+    add_above(z);
+  }
+  __device__ __forceinline__ void add_above(float z) {
+    if (fmaf(z, kz, k0) < 0.0f) {
+      const uint32_t slot = atomicAdd(n_above, 1u);
+      if (slot < static_cast<uint32_t>(kAboveCap)) above[slot] = z;
+    }
   }
 };
 
@@ -220,76 +330,39 @@ __device__ Nucleus radix_boundary(const void* row, int32_t V, int64_t h, int64_t
   return n;
 }
 
-}  // namespace
-
+// The nucleus by the three-pass method (float64 histogram relative to M,
+// exact sums above the crossing bins with their logits gathered, sorted and
+// scanned; radix refinement when the crossing bins are overfull).
 template <typename Tin>
-__global__ __launch_bounds__(kTpBlock) void topp_kernel(RowArgs a) {
-  __shared__ TpShared sh;
-  const int64_t r = blockIdx.x;
-  if (r >= a.n_rows) return;
-  constexpr int VEC = Elem<Tin>::kVec;
-  const void* row = static_cast<const Tin*>(a.logits) + r * a.row_stride;
-  const int64_t h = head_elems<Tin>(row, a.V);
-  const int64_t nvec = (a.V - h) / VEC;
-  constexpr int kLD = 4;  // loads in flight per lane: 4 to 8 with double buffering
-  vec4u v[kLD];
-  stretch_prefetch<Tin, kTpBlock, kLD>(row, h, 0, nvec, v);
-  const RowCtx cx = row_ctx<Tin>(a, r, row);
-
-  // 1. stats pass
-  Lane L;
-  lane_init(L);
-  scan_stretch<Tin, kTpBlock, 2, kLD>(row, a.V, 0, nvec, true, true, nvec, cx, L, v);
-  Partial p = block_merge<kTpBlock>(L, cx.c);
-  const uint32_t fix = rank_fixup<Tin, kTpBlock>(row, a.V, nvec, cx);
-  if (threadIdx.x == 0) {
-    sh.p = p;
-    sh.fix = fix;
-    const float P = a.top_p[r];
-    sh.active = (row_flags(a, r, p, cx.T) & (PR_FLAG_NONFINITE | PR_FLAG_BAD_TP)) == 0 && P < 1.0f;
-  }
+__device__ Nucleus legacy_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec, const Dist& D, float P,
+                                  TpShared& sh) {
+  // histogram of the candidates' masses over distance bins
   __syncthreads();
-  p = sh.p;
-  if (!sh.active) {
-    if (threadIdx.x == 0) {
-      float conf[4];
-      finalize_row(a, r, p, cx, fix, conf);
-    }
-    return;
-  }
-
-  const float T = cx.T;
-  Dist D;
-  D.M = p.m;
-  D.invT = 1.0f / T;
-  D.invT64 = 1.0 / static_cast<double>(T);
-
-  // 2. histogram of the candidates' masses over distance bins
   for (int b = threadIdx.x; b < kBins; b += kTpBlock) {
-    sh.mass[b] = 0.0;
-    sh.cnt[b] = 0;
+    sh.u.lg.mass[b] = 0.0;
+    sh.u.lg.cnt[b] = 0;
   }
   if (threadIdx.x == 0) sh.wcount = 0;
   __syncthreads();
   double s64 = 0.0, unused = 0.0;
-  for_each_logit<Tin>(row, a.V, cx.h, nvec, [&](float z) {
+  for_each_logit<Tin>(row, V, h, nvec, [&](float z) {
     const float d = D.nats(z);
     if (!(d < kDMax)) return;
     const double e = exp(D.d64(z));
     const int b = D.bin(d);
-    atomicAdd(&sh.mass[b], e);
-    atomicAdd(&sh.cnt[b], 1u);
+    atomicAdd(&sh.u.lg.mass[b], e);
+    atomicAdd(&sh.u.lg.cnt[b], 1u);
     s64 += e;
   });
   block_sum2(s64, unused, sh);  // fixed-order total: deterministic
-  const double target = static_cast<double>(a.top_p[r]) * s64;
+  const double target = static_cast<double>(P) * s64;
   const double tol = 1e-9 * s64;
 
   // crossing bins: the first bins whose cumulative mass reaches target -/+ tol
   constexpr int kPer = kBins / kTpBlock;
   const int b0 = threadIdx.x * kPer;
   double seg = 0.0;
-  for (int k = 0; k < kPer; ++k) seg += sh.mass[b0 + k];
+  for (int k = 0; k < kPer; ++k) seg += sh.u.lg.mass[b0 + k];
   const double before = block_exclusive_scan(seg, sh);
   if (threadIdx.x == 0) {
     sh.S64 = s64;
@@ -302,7 +375,7 @@ __global__ __launch_bounds__(kTpBlock) void topp_kernel(RowArgs a) {
     double c = before;
     bool lo_done = false, hi_done = false;
     for (int k = 0; k < kPer; ++k) {
-      c += sh.mass[b0 + k];
+      c += sh.u.lg.mass[b0 + k];
       if (!lo_done && c >= target - tol) {
         atomicMin(&sh.b_lo, static_cast<uint32_t>(b0 + k));
         lo_done = true;
@@ -318,16 +391,16 @@ __global__ __launch_bounds__(kTpBlock) void topp_kernel(RowArgs a) {
   uint32_t above = 0, inwin = 0;
   for (int k = 0; k < kPer; ++k) {
     const uint32_t b = static_cast<uint32_t>(b0 + k);
-    if (b < b_lo) above += sh.cnt[b];
-    else if (b <= b_hi) inwin += sh.cnt[b];
+    if (b < b_lo) above += sh.u.lg.cnt[b];
+    else if (b <= b_hi) inwin += sh.u.lg.cnt[b];
   }
   above = block_sum_u(above, sh);
   inwin = block_sum_u(inwin, sh);
 
-  // 3. exact sums above the crossing bins; gather the crossing bins' logits
+  // exact sums above the crossing bins; gather the crossing bins' logits
   double mA = 0.0, eA = 0.0;
   const bool gather = inwin <= static_cast<uint32_t>(kCap);
-  for_each_logit<Tin>(row, a.V, cx.h, nvec, [&](float z) {
+  for_each_logit<Tin>(row, V, h, nvec, [&](float z) {
     const float d = D.nats(z);
     if (!(d < kDMax)) return;
     const uint32_t b = static_cast<uint32_t>(D.bin(d));
@@ -351,7 +424,7 @@ __global__ __launch_bounds__(kTpBlock) void topp_kernel(RowArgs a) {
 
   Nucleus nuc;
   if (gather) {
-    // 4. sort the crossing logits (descending) and scan their masses
+    // sort the crossing logits (descending) and scan their masses
     const int nw = static_cast<int>(sh.wcount < static_cast<uint32_t>(kCap) ? sh.wcount : kCap);
     int n2 = 2;
     while (n2 < nw) n2 <<= 1;
@@ -410,8 +483,261 @@ __global__ __launch_bounds__(kTpBlock) void topp_kernel(RowArgs a) {
       nuc.E = sh.EN;
     }
   } else {
-    nuc = radix_boundary<Tin>(row, a.V, cx.h, nvec, D, sh);
+    nuc = radix_boundary<Tin>(row, V, h, nvec, D, sh);
   }
+  return nuc;
+}
+
+// The nucleus from the stats-pass histogram and one exact pass. Returns
+// false (and leaves nuc unset) when the row must take the three-pass method.
+template <typename Tin>
+__device__ bool hist_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec, const Dist& D, float P,
+                             float A0, const HistHook& hk, TpShared& sh, Nucleus& nuc) {
+  const double* tab = sh.exptab;
+  const uint32_t n_above = sh.n_above;
+  if (n_above > static_cast<uint32_t>(kAboveCap)) return false;
+
+  // 1. the window of bins around P * (total): a logit of bin b lies at
+  // (b + 1/2 + delta) / kHK - kHAbove nats below A0; with w = 1/kHK the bin's
+  // mass is mass(centre) * sum exp(-delta w) ~ mass(centre) * (count - w *
+  // sum delta) (second-order error below count * w^2 / 8). Masses relative
+  // to M.
+  const double lead = (static_cast<double>(A0) - static_cast<double>(D.M)) * D.invT64 + kHAbove;
+  double sa = 0.0;
+  for (uint32_t i = threadIdx.x; i < n_above; i += kTpBlock) sa += exp_tang(D.d64(sh.above[i]), tab);
+  constexpr int kPer = kHB / kTpBlock;
+  const int b0 = threadIdx.x * kPer;
+  double wb[kPer];
+  double seg = 0.0;
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const double w = exp(lead - (static_cast<double>(b0 + k) + 0.5) / kHK);
+    const double dsum = static_cast<double>(sh.u.hs.off[b0 + k]) / kOffQ;
+    wb[k] = (static_cast<double>(sh.u.hs.cnt[b0 + k]) - dsum / kHK) * w;
+    seg += wb[k];
+  }
+  double tot = seg;
+  block_sum2(sa, tot, sh);
+  tot += sa;
+  const double t_lo = static_cast<double>(P) * tot * (1.0 - kWinMargin);
+  const double t_hi = static_cast<double>(P) * tot * (1.0 + kWinMargin);
+  const double before = sa + block_exclusive_scan(seg, sh);
+  if (threadIdx.x == 0) {
+    sh.hb_lo = kHB - 1;
+    sh.hb_hi = kHB - 1;
+  }
+  __syncthreads();
+  {
+    double c = before;
+    bool lo_done = false, hi_done = false;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+      c += wb[k];
+      if (!lo_done && c >= t_lo) {
+        atomicMin(&sh.hb_lo, b0 + k);
+        lo_done = true;
+      }
+      if (!hi_done && c >= t_hi) {
+        atomicMin(&sh.hb_hi, b0 + k);
+        hi_done = true;
+      }
+    }
+  }
+  if (threadIdx.x == 0) sh.wcount = 0;
+  __syncthreads();
+  const int b_lo = sa >= t_lo ? -1 : sh.hb_lo;  // -1: the list above the bins
+  const int b_hi = sa >= t_hi ? -1 : sh.hb_hi;
+  uint32_t inwin = 0, above = 0;
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int b = b0 + k;
+    if (b < b_lo) above += sh.u.hs.cnt[b];
+    else if (b <= b_hi) inwin += sh.u.hs.cnt[b];
+  }
+  inwin = block_sum_u(inwin, sh) + (b_lo < 0 ? n_above : 0u);
+  above = block_sum_u(above, sh) + (b_lo >= 0 ? n_above : 0u);  // counts are exact
+  if (inwin > static_cast<uint32_t>(kCap)) return false;
+  // The counts are consumed: the same LDS now holds exp(centre of bin b - M).
+  // A logit of bin b is exp(dd) = wtab[b] * exp(dd - centre), and |dd - centre|
+  // is at most half a bin (0.0092 nats) plus the float32 rounding of bf:
+  // degree-5 Taylor polynomial (truncation below 1e-14 while |dd - centre| <
+  // 0.02; otherwise, and for the list, the table-driven exp).
+  const double invK = 1.0 / static_cast<double>(kHK);
+  const double c0 = lead - 0.5 * invK;  // centre of bin b: c0 - b * invK
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) sh.u.wtab[b0 + k] = exp(fma(-static_cast<double>(b0 + k), invK, c0));
+  __syncthreads();
+
+  // 2. exact pass: sums above the window, the window gathered, the total
+  double mA = 0.0, eA = 0.0, sT = 0.0;
+  const double M64 = static_cast<double>(D.M);
+  for_each_logit<Tin>(row, V, h, nvec, [&](float z) {
+    const float bf = fmaf(z, hk.kz, hk.k0);
+    if (!(bf < static_cast<float>(kHB))) return;  // beyond 50 nats below A0, -inf, NaN
+    const int b = bf < 0.0f ? -1 : static_cast<int>(bf);
+    const double dd = (static_cast<double>(z) - M64) * D.invT64;
+    const double r = dd - fma(-static_cast<double>(b < 0 ? 0 : b), invK, c0);
+    double e;
+    if (b >= 0 && fabs(r) < 0.02) {
+      double q = fma(r, 1.0 / 120.0, 1.0 / 24.0);
+      q = fma(q, r, 1.0 / 6.0);
+      q = fma(q, r, 0.5);
+      q = fma(q, r, 1.0);
+      q = fma(q, r, 1.0);
+      e = sh.u.wtab[b] * q;
+    } else {  // the list above the bins, or a bin far off through float32 rounding of bf (huge logits)
+      e = exp_tang(fmax(dd, -700.0), tab);
+    }
+    const bool ab = b < b_lo;
+    const double fa = ab ? 1.0 : 0.0;
+    mA = fma(e, fa, mA);
+    eA = fma(e * dd, fa, eA);
+    sT += dd > -static_cast<double>(kDMax) ? e : 0.0;
+    if (!ab && b <= b_hi) {
+      const uint32_t slot = atomicAdd(&sh.wcount, 1u);
+      if (slot < static_cast<uint32_t>(kCap)) sh.win[slot] = z;
+    }
+  });
+  block_sum2(mA, eA, sh);
+  double sT2 = sT, unused = 0.0;
+  block_sum2(sT2, unused, sh);
+  const uint32_t cA = above;
+  const uint32_t nw_all = sh.wcount;
+  if (nw_all > static_cast<uint32_t>(kCap)) return false;
+
+  // 3. sort the window (descending), scan its masses, verify the crossing
+  const int nw = static_cast<int>(nw_all);
+  int n2 = 2;
+  while (n2 < nw) n2 <<= 1;
+  for (int i = nw + threadIdx.x; i < n2; i += kTpBlock) sh.win[i] = -INFINITY;
+  __syncthreads();
+  bitonic_desc(sh.win, n2);
+  const int per = (n2 + kTpBlock - 1) / kTpBlock;
+  const int i0 = threadIdx.x * per;
+  const int i1 = i0 + per < nw ? i0 + per : nw;
+  double sm = 0.0, se = 0.0;
+  for (int i = i0; i < i1; ++i) {
+    const double dd = D.d64(sh.win[i]);
+    const double e = exp_tang(dd, tab);
+    sm += e;
+    se += e * dd;
+  }
+  const double cm = block_exclusive_scan(sm, sh);
+  const double ce = block_exclusive_scan(se, sh);
+  double wm = sm, we = se;
+  block_sum2(wm, we, sh);
+  const double S = sT2;  // every logit within 50 nats of M
+  const double target = static_cast<double>(P) * S;
+  if (!(mA < target) || mA + wm < target) return false;  // crossing outside the window
+  if (threadIdx.x == 0) sh.jfirst = 0xffffffffu;
+  __syncthreads();
+  double run_m = mA + cm;
+  for (int i = i0; i < i1; ++i) {
+    run_m += exp_tang(D.d64(sh.win[i]), tab);
+    if (run_m >= target) {
+      atomicMin(&sh.jfirst, static_cast<uint32_t>(i));
+      break;
+    }
+  }
+  __syncthreads();
+  const uint32_t jf = sh.jfirst;
+  if (jf == 0xffffffffu) return false;
+  if (static_cast<int>(jf) >= i0 && static_cast<int>(jf) < i1) {
+    double m2 = mA + cm, e2 = eA + ce;
+    for (int i = i0; i <= static_cast<int>(jf); ++i) {
+      const double dd = D.d64(sh.win[i]);
+      const double e = exp_tang(dd, tab);
+      m2 += e;
+      e2 += e * dd;
+    }
+    sh.SN = m2;
+    sh.EN = e2;
+  }
+  __syncthreads();
+  nuc.k = static_cast<int32_t>(cA + jf + 1);
+  nuc.S = sh.SN;
+  nuc.E = sh.EN;
+  return true;
+}
+
+}  // namespace
+
+template <typename Tin>
+__global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) void topp_kernel(RowArgs a) {
+  __shared__ TpShared sh;
+  const int64_t r = blockIdx.x;
+  if (r >= a.n_rows) return;
+  constexpr int VEC = Elem<Tin>::kVec;
+  const void* row = static_cast<const Tin*>(a.logits) + r * a.row_stride;
+  const int64_t h = head_elems<Tin>(row, a.V);
+  const int64_t nvec = (a.V - h) / VEC;
+  constexpr int kLD = 4;  // loads in flight per lane: 4 to 8 with double buffering
+  vec4u v[kLD];
+  stretch_prefetch<Tin, kTpBlock, kLD>(row, h, 0, nvec, v);
+  const RowCtx cx = row_ctx<Tin>(a, r, row);
+
+  // Anchor of the histogram: the largest of the prefetched logits. The
+  // histogram and the list are cleared meanwhile.
+  float pm = -INFINITY;
+#pragma unroll
+  for (int u = 0; u < kLD; ++u) {
+    float z[VEC];
+    Elem<Tin>::unpack(v[u], z);
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) pm = fmaxf(pm, z[k]);
+  }
+  pm = wave_max(pm);
+  for (int b = threadIdx.x; b < kHB + kWave; b += kTpBlock) {
+    sh.u.hs.cnt[b] = 0u;
+    sh.u.hs.off[b] = 0;
+  }
+  if (threadIdx.x < 64) sh.exptab[threadIdx.x] = exp2(static_cast<double>(threadIdx.x) * (1.0 / 64.0));
+  if (threadIdx.x == 0) sh.n_above = 0;
+  if (threadIdx.x % kWave == 0) sh.red_f[threadIdx.x / kWave] = pm;
+  __syncthreads();
+  float A0 = sh.red_f[0];
+  for (int k = 1; k < kNW; ++k) A0 = fmaxf(A0, sh.red_f[k]);
+  const bool anchored = A0 > -INFINITY && A0 < INFINITY && temperature_ok(cx.T);
+  const float invT = 1.0f / cx.T;
+  HistHook hk;
+  hk.cnt = sh.u.hs.cnt;
+  hk.off = sh.u.hs.off;
+  hk.above = sh.above;
+  hk.n_above = &sh.n_above;
+  hk.kz = anchored ? -invT * kHK : 0.0f;
+  hk.k0 = anchored ? fmaf(A0, invT * kHK, kHAbove * kHK) : INFINITY;  // unanchored: nothing binned
+
+  // 1. stats pass, building the histogram
+  Lane L;
+  lane_init(L);
+  scan_stretch<Tin, kTpBlock, 2, kLD, false>(row, a.V, 0, nvec, true, true, nvec, cx, L, v, hk);
+  Partial p = block_merge<kTpBlock>(L, cx.c);
+  const uint32_t fix = rank_fixup<Tin, kTpBlock>(row, a.V, nvec, cx);
+  if (threadIdx.x == 0) {
+    sh.p = p;
+    sh.fix = fix;
+    const float P = a.top_p[r];
+    sh.active = (row_flags(a, r, p, cx.T) & (PR_FLAG_NONFINITE | PR_FLAG_BAD_TP)) == 0 && P < 1.0f;
+  }
+  __syncthreads();
+  p = sh.p;
+  if (!sh.active) {
+    if (threadIdx.x == 0) {
+      float conf[4];
+      finalize_row(a, r, p, cx, fix, conf);
+    }
+    return;
+  }
+
+  const float T = cx.T;
+  Dist D;
+  D.M = p.m;
+  D.invT = 1.0f / T;
+  D.invT64 = 1.0 / static_cast<double>(T);
+  const float P = a.top_p[r];
+  Nucleus nuc;
+  if (!(anchored && hist_nucleus<Tin>(row, a.V, cx.h, nvec, D, P, A0, hk, sh, nuc)))
+    nuc = legacy_nucleus<Tin>(row, a.V, cx.h, nvec, D, P, sh);
   if (threadIdx.x == 0) {
     float conf[4];
     finalize_row(a, r, p, cx, fix, conf, &nuc);
