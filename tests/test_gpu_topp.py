@@ -74,6 +74,31 @@ def test_topp_massive_ties_radix_path(V):
     compare_features(gpu_features(logits, ids, T, P), oracle_features(logits, ids, T, P))
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_topp_histogram_edge_rows(dtype):
+    """Rows aimed at each branch of the two-read method: no finite anchor
+    (the first vectors all -inf), more logits far above the anchor than the
+    list holds, a crossing inside that list (one dominant spike), a nucleus
+    spanning the list and the bins, and a near-flat row with a wide window."""
+    V = 65536
+    rng = np.random.default_rng(77)
+    rows, ids, Ts, Ps = [], [], [], []
+    def add(z, y, T, P):
+        rows.append(np.asarray(z, dtype=np.float64)); ids.append(int(y)); Ts.append(T); Ps.append(P)
+    z = rng.normal(0, 2, V); z[:20000] = -np.inf
+    add(z, 30000, 1.0, 0.9)                                  # no finite anchor among the first vectors
+    z = rng.normal(0, 1, V); z[40000:41000] = 40.0 + rng.normal(0, 1, 1000)
+    add(z, 40500, 1.0, 0.9)                                  # 1,000 logits ~40 nats above the anchor
+    z = rng.normal(0, 1, V); z[50000] = 120.0
+    add(z, 50000, 1.0, 0.9)                                  # one spike: nucleus = {spike}
+    z = rng.normal(0, 1, V); z[60000] = 42.0
+    add(z, 123, 4.0, 0.95)                                   # spike 10 nats above the bulk at T = 4
+    add(rng.normal(0, 0.01, V), 5, 1.2, 0.93)                # near-flat: wide window
+    logits, ids, T, P = _run(np.stack(rows), ids, Ts, Ps, dtype)
+    print(f"case topp histogram edges {dtype}", flush=True)
+    compare_features(gpu_features(logits, ids, T, P), oracle_features(logits, ids, T, P))
+
+
 def test_topp_workload_scaled():
     """The top-p row model (V = 262,144 float32, T ~ U[0.3,1.2], P ~ U[0.8,0.95]) on a few requests."""
     w = wl.scaled(wl.WORKLOADS["topp_128x256_v262144_f32"], n_req=4, len_hi=6, len_lo=6)
