@@ -338,9 +338,9 @@ def main():
     if os.path.exists(args.traffic_json):
         try:
             t = json.load(open(args.traffic_json)).get(w.name)
-            if t and t.get("kernel_source_hash") == kernel_source_hash():
+            if t and t.get("kernel_source_hash") == kernel_source_hash(t.get("kernel", "")):
                 traffic = t["bytes_per_launch"]
-        except (OSError, ValueError):
+        except (OSError, ValueError, KeyError):
             traffic = None
 
     result = {
@@ -375,14 +375,24 @@ def main():
     print(json.dumps(result), flush=True)
 
 
-def kernel_source_hash() -> str:
-    """Hash of the kernel sources: stored counter traffic is only valid for the same kernels."""
+# Sources each measured kernel is compiled from (its own file and every header it includes).
+KERNEL_SOURCES = {
+    "row_features_kernel": ("include/prouter.h", "paper_2608_28726_amd/csrc/device_util.h",
+                            "paper_2608_28726_amd/csrc/row_features.h", "paper_2608_28726_amd/csrc/row_scan.h",
+                            "paper_2608_28726_amd/csrc/row_features.hip"),
+    "topp_kernel": ("include/prouter.h", "paper_2608_28726_amd/csrc/device_util.h",
+                    "paper_2608_28726_amd/csrc/row_features.h", "paper_2608_28726_amd/csrc/row_scan.h",
+                    "paper_2608_28726_amd/csrc/topp.h", "paper_2608_28726_amd/csrc/topp.hip"),
+}
+
+
+def kernel_source_hash(kernel: str) -> str:
+    """Hash of one kernel's sources: stored counter traffic is only valid for the same kernel."""
     import hashlib
-    d = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_28726_amd", "csrc")
+    root = os.path.dirname(os.path.abspath(__file__))
     h = hashlib.sha256()
-    for fn in sorted(os.listdir(d)):
-        if fn.endswith((".hip", ".h")):
-            h.update(open(os.path.join(d, fn), "rb").read())
+    for fn in KERNEL_SOURCES[kernel]:
+        h.update(open(os.path.join(root, fn), "rb").read())
     return h.hexdigest()[:16]
 
 

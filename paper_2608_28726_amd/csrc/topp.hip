@@ -31,7 +31,8 @@
 // three-pass method: a 4096-bin float64 histogram relative to M, exact sums
 // above the crossing bins with their logits gathered, sorted and scanned,
 // and for overfull crossing bins a byte-wise radix refinement over
-// order-preserving keys (four more reads) that resolves ties by counting.
+// order-preserving keys (four more reads, and one for exact sums above the
+// boundary value) that resolves ties by counting.
 #include "topp.h"
 
 #include "row_scan.h"
@@ -262,10 +263,14 @@ __device__ void bitonic_desc(float* a, int n2) {
 
 // Radix refinement inside the crossing bins [b_lo, b_hi]: finds the boundary
 // logit value and resolves ties by count. On entry sh.massAbove/Eabove/
-// cntAbove hold the exact sums of the logits above b_lo.
+// cntAbove hold the exact sums of the logits above b_lo. The digit masses
+// are float atomics and only choose the digits; the masses that reach the
+// result are summed again in a fixed order once the boundary value is known.
 template <typename Tin>
 __device__ Nucleus radix_boundary(const void* row, int32_t V, int64_t h, int64_t nvec, const Dist& D, TpShared& sh) {
-  double massGT = sh.massAbove, EGT = sh.Eabove;
+  const double massAbove0 = sh.massAbove, Eabove0 = sh.Eabove;
+  const uint32_t blo = sh.b_lo, bhi = sh.b_hi;
+  double massGT = massAbove0, EGT = Eabove0;
   uint32_t cntGT = sh.cntAbove;
   uint32_t prefix = 0, mask = 0, cnt_last = 0;
   for (int pass = 0; pass < 4; ++pass) {
@@ -276,7 +281,6 @@ __device__ Nucleus radix_boundary(const void* row, int32_t V, int64_t h, int64_t
       sh.rcnt[b] = 0;
     }
     __syncthreads();
-    const uint32_t blo = sh.b_lo, bhi = sh.b_hi;
     for_each_logit<Tin>(row, V, h, nvec, [&](float z) {
       const float d = D.nats(z);
       if (!(d < kDMax)) return;
@@ -314,6 +318,24 @@ __device__ Nucleus radix_boundary(const void* row, int32_t V, int64_t h, int64_t
     cntGT = sh.cntAbove;
     cnt_last = sh.rcount;
     __syncthreads();
+  }
+  // Exact sums over the crossing bins' logits above z* (larger keys), each
+  // lane in its own fixed order, then a fixed-order block sum.
+  {
+    double gm = 0.0, ge = 0.0;
+    for_each_logit<Tin>(row, V, h, nvec, [&](float z) {
+      const float d = D.nats(z);
+      if (!(d < kDMax)) return;
+      const uint32_t b = static_cast<uint32_t>(D.bin(d));
+      if (b < blo || b > bhi || float_key(z) <= prefix) return;
+      const double dd = D.d64(z);
+      const double e = exp(dd);
+      gm += e;
+      ge += e * dd;
+    });
+    block_sum2(gm, ge, sh);
+    massGT = massAbove0 + gm;
+    EGT = Eabove0 + ge;
   }
   // All remaining candidates share the value z*: equal masses e*.
   const float zs = key_float(prefix);

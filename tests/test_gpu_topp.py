@@ -74,6 +74,24 @@ def test_topp_massive_ties_radix_path(V):
     compare_features(gpu_features(logits, ids, T, P), oracle_features(logits, ids, T, P))
 
 
+def test_topp_deterministic():
+    """Two runs give bit-identical outputs on every path: the two-read
+    method (random rows), the three-pass fallback (near-flat row) and its
+    radix refinement (tie-heavy rows), whose float atomics only choose bins
+    and digits."""
+    V = 151936
+    rng = np.random.default_rng(5)
+    rows = [rng.normal(0, 2, V), rng.normal(0, 0.01, V), np.zeros(V), rng.choice([0.0, 0.5, 1.0], size=V)]
+    ids = [int(rng.integers(0, V)) for _ in rows]
+    logits, ids, T, P = _run(np.stack(rows), ids, [0.8, 1.2, 1.0, 0.9], [0.9, 0.93, 0.37, 0.8], torch.bfloat16)
+    print("case topp deterministic", flush=True)
+    a1 = gpu_features(logits, ids, T, P)
+    a2 = gpu_features(logits, ids, T, P)
+    for k in a1:
+        assert np.array_equal(a1[k].view(np.uint32), a2[k].view(np.uint32)), k
+    compare_features(a1, oracle_features(logits, ids, T, P))
+
+
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_topp_histogram_edge_rows(dtype):
     """Rows aimed at each branch of the two-read method: no finite anchor
