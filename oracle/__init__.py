@@ -12,9 +12,12 @@ ship rule p >= tau):
   vocabulary logit row after temperature and optional top-p.
 * :mod:`oracle.aggregate` -- per-request aggregation of those features
   over a ragged batch, the summary score and the ship-or-escalate rule.
+* :mod:`oracle.sequence` -- the paper's own verifier input: the top-K
+  entropy (K = 20) and the stacked per-token tuples (l, m, h, rho).
 
 Parity pinning: every function here is pinned by ``tests/test_oracle_pins.py``
-against closed forms, invariants and pure-Python brute force, except the
+and ``tests/test_oracle_sequence.py`` against closed forms, invariants and
+pure-Python brute force, except the
 default score head (a fixed linear summary chosen because the paper
 publishes no trained head weights), which is *parity unpinned* against the
 paper.
@@ -34,4 +37,11 @@ from .aggregate import (  # noqa: F401
     request_aggregate,
     route,
     score_from_aggregates,
+)
+from .sequence import (  # noqa: F401
+    PAPER_TOP_K,
+    feature_sequence,
+    position_fraction,
+    topk_entropy,
+    topk_entropy_batch,
 )
