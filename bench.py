@@ -33,6 +33,9 @@ def parse_args():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="ragged_64req_v151936_bf16")
+    ap.add_argument("--path", choices=("features", "sequence"), default="features",
+                    help="features: per-token features, per-request summaries and route (the default); "
+                         "sequence: the paper's verifier input sequence (l, m, top-20 entropy, t/T) per token")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="time budget of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
@@ -65,6 +68,51 @@ def copy_probe(torch, nbytes=1 << 30, reps=10):
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / reps
     return {"bytes_read": nbytes, "bytes_written": nbytes, "ms": ms, "gb_per_s": 2 * nbytes / ms / 1e6}
+
+
+def cpu_baseline_sequence(torch, batch, X_gpu, seconds, top_k):
+    """The fp64 oracle of the verifier input sequence on the first rows of the
+    batch (per-token features, top-K entropy, position fraction), time-bounded,
+    one core."""
+    import oracle
+    from oracle import sequence as oseq
+    from paper_2608_28726_amd import workloads as wl
+    w = batch.workload
+    n_max = min(batch.n_rows, 4096)
+    raw = wl.to_host_raw(batch.logits[:n_max])
+    ids = batch.sampled_ids[:n_max].cpu().numpy()
+    T = batch.temperature[:n_max].cpu().numpy()
+    P = None if batch.top_p is None else batch.top_p[:n_max].cpu().numpy()
+    dtype = "bf16" if w.dtype == "bf16" else "f32"
+    rho = oseq.position_fraction(batch.offsets)
+    rows = []
+    t0 = time.perf_counter()
+    while len(rows) < n_max and (len(rows) < 16 or time.perf_counter() - t0 < seconds):
+        r = len(rows)
+        Pr = None if P is None else float(P[r])
+        f = oracle.token_features(raw[r], dtype, int(ids[r]), float(T[r]), Pr)
+        h = -oseq.topk_entropy(raw[r], dtype, float(T[r]), Pr, top_k)
+        rows.append((f["logprob"], f["maxprob"], h, rho[r]))
+    elapsed = time.perf_counter() - t0
+    n = len(rows)
+    Xo = np.array(rows, dtype=np.float64)
+    Xg = X_gpu[:n].cpu().numpy().astype(np.float64)
+    with np.errstate(invalid="ignore"):
+        ok = (np.abs(Xg - Xo) <= 1e-5 + 1e-4 * np.abs(Xo)) | (np.isnan(Xg) & np.isnan(Xo)) | (Xg == Xo)
+    bad = int((~ok).sum())
+    if bad:
+        i = np.argwhere(~ok)[:3].tolist()
+        log(f"[bench] parity detail: {i} gpu {[Xg[a, b] for a, b in i]} oracle {[Xo[a, b] for a, b in i]}")
+    return {
+        "value": n / elapsed,
+        "unit": "rows/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"first {n} rows of the same batch: the verifier input tuple (log-prob, max-prob, top-{top_k} "
+                  f"entropy, position fraction) in float64; {elapsed:.1f} s on 1 host core (numpy, single-threaded)",
+        "parity_mismatches": bad,
+        "rows": n,
+    }
 
 
 def cpu_baseline(torch, batch, feats_gpu, seconds):
@@ -148,10 +196,14 @@ def run_offline(args, torch, pr, wl, w):
     log(f"[bench] {w.name}: {n_rows} rows in {n_chunks} chunk(s), {copies} rotating copies, "
         f"{n_rows * w.V * w.elem_bytes / 1e9:.2f} GB per step")
     offs = [torch.as_tensor(b.offsets).cuda() for b in batches]
-    feats = [pr.token_features(b.logits, b.sampled_ids, b.temperature, b.top_p) for b in batches]
+    sequence = args.path == "sequence"
+    if sequence:
+        feats = [torch.empty(b.n_rows, 4, dtype=torch.float32, device="cuda") for b in batches]
+    else:
+        feats = [pr.token_features(b.logits, b.sampled_ids, b.temperature, b.top_p) for b in batches]
     wss = []
     for b in batches:
-        nb = pr.token_features_workspace(b.logits, b.top_p is not None)
+        nb = 0 if sequence else pr.token_features_workspace(b.logits, b.top_p is not None)
         wss.append(torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda"))
     state = {"k": 0}
 
@@ -163,11 +215,17 @@ def run_offline(args, torch, pr, wl, w):
             b = batches[c]
             if ev is not None and c == group[0]:
                 ev[0].record()
-            pr.token_features(b.logits, b.sampled_ids, b.temperature, b.top_p, out=feats[c], workspace=wss[c])
+            if sequence:
+                pr.feature_sequence(b.logits, b.sampled_ids, b.temperature, offs[c], top_p=b.top_p,
+                                    top_k=pr.PAPER_TOP_K, out=feats[c])
+            else:
+                pr.token_features(b.logits, b.sampled_ids, b.temperature, b.top_p, out=feats[c],
+                                  workspace=wss[c])
             if ev is not None and c == group[-1]:
                 ev[1].record()
-            agg = pr.request_aggregate(feats[c], offs[c], q=w.q)
-            out = pr.route(agg["score"], w.tau)
+            if not sequence:
+                agg = pr.request_aggregate(feats[c], offs[c], q=w.q)
+                out = pr.route(agg["score"], w.tau)
         return out
 
     for _ in range(args.warmup):
@@ -177,12 +235,17 @@ def run_offline(args, torch, pr, wl, w):
     log(f"[bench] timing {args.steps} steps")
     t0 = time.perf_counter()
     for k in range(args.steps):
-        ship, n_ship = step(events[k])
+        step(events[k])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     kern_ms = float(np.mean([a.elapsed_time(b) for a, b in events]))
-    bytes_launch = n_rows * algorithmic_bytes_per_row(w.V, w.elem_bytes)
+    if sequence:  # one read of the row, id and temperature in, the 16-byte tuple out
+        bytes_launch = n_rows * (w.V * w.elem_bytes + 4 + 4 + 16)
+    else:
+        bytes_launch = n_rows * algorithmic_bytes_per_row(w.V, w.elem_bytes)
     kernel = "topp_kernel" if w.P_lo is not None else "row_features_kernel"
+    if sequence:
+        kernel += " (sequence variant)"
     if n_chunks > 1:  # events bracket all chunks' row kernels and their summaries
         kernel += f" x{n_chunks} chunks (+summaries)"
     extra = {"kernel": kernel, "kernel_ms": kern_ms, "bytes_per_launch": bytes_launch}
@@ -337,7 +400,7 @@ def main():
     traffic = None
     if os.path.exists(args.traffic_json):
         try:
-            t = json.load(open(args.traffic_json)).get(w.name)
+            t = json.load(open(args.traffic_json)).get(traffic_key(w.name, args.path))
             if t and t.get("kernel_source_hash") == kernel_source_hash(t.get("kernel", "")):
                 traffic = t["bytes_per_launch"]
         except (OSError, ValueError, KeyError):
@@ -358,6 +421,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "n_req": w.n_req, "rows": n_rows, "V": w.V, "logits": w.dtype,
                    "mode": "streaming decode, one step per token" if stream_mode else "offline ragged batch",
+                   "path": "verifier input sequence (l, m, top-20 entropy, t/T)" if args.path == "sequence"
+                   else "features, summaries, route",
                    "temperature": [w.T_lo, w.T_hi], "top_p": None if w.P_lo is None else [w.P_lo, w.P_hi],
                    "aggregation": f"mean/min/q={w.q} nearest-rank", "threshold": w.tau},
         "gb_per_s": achieved,
@@ -369,7 +434,10 @@ def main():
         result["copy_probe"] = copy_probe(torch)
     if not args.no_cpu_baseline and batch is not None:
         log("[bench] timing the oracle on the host")
-        result["cpu_baseline"] = cpu_baseline(torch, batch, feats, args.cpu_seconds)
+        if args.path == "sequence":
+            result["cpu_baseline"] = cpu_baseline_sequence(torch, batch, feats, args.cpu_seconds, pr.PAPER_TOP_K)
+        else:
+            result["cpu_baseline"] = cpu_baseline(torch, batch, feats, args.cpu_seconds)
         log(f"[bench] oracle {result['cpu_baseline']['value']:.1f} rows/s, "
             f"parity mismatches {result['cpu_baseline']['parity_mismatches']}")
     print(json.dumps(result), flush=True)
@@ -379,11 +447,17 @@ def main():
 KERNEL_SOURCES = {
     "row_features_kernel": ("include/prouter.h", "paper_2608_28726_amd/csrc/device_util.h",
                             "paper_2608_28726_amd/csrc/row_features.h", "paper_2608_28726_amd/csrc/row_scan.h",
-                            "paper_2608_28726_amd/csrc/row_features.hip"),
+                            "paper_2608_28726_amd/csrc/topk.h", "paper_2608_28726_amd/csrc/row_features.hip"),
     "topp_kernel": ("include/prouter.h", "paper_2608_28726_amd/csrc/device_util.h",
                     "paper_2608_28726_amd/csrc/row_features.h", "paper_2608_28726_amd/csrc/row_scan.h",
-                    "paper_2608_28726_amd/csrc/topp.h", "paper_2608_28726_amd/csrc/topp.hip"),
+                    "paper_2608_28726_amd/csrc/topk.h", "paper_2608_28726_amd/csrc/topp.h",
+                    "paper_2608_28726_amd/csrc/topp.hip"),
 }
+
+
+def traffic_key(workload: str, path: str) -> str:
+    """Key of a workload's stored counter traffic (one entry per measured path)."""
+    return workload if path == "features" else f"{workload}:{path}"
 
 
 def kernel_source_hash(kernel: str) -> str:

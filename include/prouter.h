@@ -147,6 +147,41 @@ pr_status pr_token_features(const void* logits, pr_dtype dtype, int64_t n_rows, 
                             const float* top_p, const pr_token_features_t* out, void* workspace,
                             size_t workspace_bytes, void* stream);
 
+/* Largest K of pr_feature_sequence's top-K entropy. */
+#define PR_MAX_TOP_K 32
+
+/*
+ * The paper's verifier input sequence X (Sec. 3.1, Eq. 3 and the text after
+ * it). Request i owns rows offsets[i] .. offsets[i+1]-1; row r is its token
+ * t = r - offsets[i] + 1 of T_i = offsets[i+1] - offsets[i]. For every row:
+ *   X[r][0] = l_t   = log p(y_t)               (logprob of pr_token_features)
+ *   X[r][1] = m_t   = max_v p(v)               (maxprob)
+ *   X[r][2] = h_t   = -H_t, H_t = -sum of p(v) log p(v) over the top_k most
+ *                     probable tokens, p not renormalised over them
+ *   X[r][3] = rho_t = t / T_i
+ * p is the distribution after temperature and top-p, as in pr_token_features;
+ * when the nucleus holds fewer than top_k tokens, H_t sums over the nucleus.
+ * Tokens of probability 0 (logit -inf) add nothing.
+ *   logits .. top_p  as for pr_token_features.
+ *   offsets    int32 [n_req + 1], device: offsets[0] == 0, non-decreasing,
+ *              offsets[n_req] == n_rows (a precondition, as for
+ *              pr_request_aggregate; pr_validate_offsets checks it). A row
+ *              outside the offsets gets rho = NaN.
+ *   top_k      1 .. PR_MAX_TOP_K (the paper uses 20).
+ *   X          float [n_rows][4], device, row-major.
+ *   features   host pointer to a struct of device arrays that also receive
+ *              the per-token features of pr_token_features (all members
+ *              set), or NULL. Their flags give the reason of NaN entries: a
+ *              row flagged PR_FLAG_NONFINITE or PR_FLAG_BAD_TP has NaN in
+ *              l, m and h; PR_FLAG_BAD_ID makes l NaN only.
+ * One workgroup reads each row once; no workspace. n_rows == 0 launches
+ * nothing.
+ */
+pr_status pr_feature_sequence(const void* logits, pr_dtype dtype, int64_t n_rows, int32_t vocab,
+                              int64_t row_stride, const int32_t* sampled_ids, const float* temperature,
+                              const float* top_p, const int32_t* offsets, int32_t n_req, int32_t top_k,
+                              float* X, const pr_token_features_t* features, void* stream);
+
 /*
  * Ragged per-request summaries and score (Sec. 3.1, the stacked feature
  * sequence X; Sec. 4.2, Table "ablation", quantile-summary input).

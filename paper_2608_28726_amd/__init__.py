@@ -9,6 +9,9 @@ stream. PyTorch only provides device memory and streams here.
     agg = request_aggregate(feats, offsets)
     ship, n_ship = route(agg["score"], threshold)
 
+The paper's own verifier input, the per-token tuples (l, m, h, rho) with the
+top-K entropy (Sec. 3.1, Eq. 3): :func:`feature_sequence`.
+
 Streaming decode: :class:`StreamState`.
 """
 
@@ -22,8 +25,10 @@ from . import _abi
 from ._abi import (FLAG_BAD_ID, FLAG_BAD_TP, FLAG_NONFINITE, FLAG_OUTSIDE_NUCLEUS,  # noqa: F401
                    ProuterError)
 
-__all__ = ["token_features", "request_aggregate", "route", "validate_offsets", "StreamState",
-           "token_features_workspace", "ProuterError", "FEATURE_FLOATS", "FEATURE_INTS"]
+__all__ = ["token_features", "feature_sequence", "request_aggregate", "route", "validate_offsets", "StreamState",
+           "token_features_workspace", "ProuterError", "FEATURE_FLOATS", "FEATURE_INTS", "PAPER_TOP_K"]
+
+PAPER_TOP_K = 20  # K of the paper's top-K entropy (Sec. 3.1)
 
 FEATURE_FLOATS = ("max_logit", "lse", "entropy", "logprob", "maxprob", "margin")
 FEATURE_INTS = ("rank", "argmax", "cutoff")
@@ -104,6 +109,36 @@ def token_features(logits: torch.Tensor, sampled_ids: torch.Tensor, temperature,
                              _stream_handle())
     _abi.check("pr_token_features", st)
     return out
+
+
+def feature_sequence(logits: torch.Tensor, sampled_ids: torch.Tensor, temperature, offsets: torch.Tensor,
+                     top_p=None, top_k: int = PAPER_TOP_K, features: bool = False, out: torch.Tensor | None = None):
+    """The paper's verifier input sequence X (``pr_feature_sequence``).
+
+    Returns X, a float32 [n_rows, 4] tensor of (log-prob of the sampled token,
+    max probability, negated top-K entropy, position fraction t / T) per
+    row; request i owns rows ``offsets[i]:offsets[i+1]``. With
+    ``features=True`` returns ``(X, feats)``, feats being the dict that
+    :func:`token_features` returns, computed in the same pass. ``out``: an
+    optional float32 [n_rows, 4] CUDA tensor that receives X.
+    """
+    n, V = logits.shape
+    temperature = _as_row_tensor(temperature, n, logits.device)
+    top_p = None if top_p is None else _as_row_tensor(top_p, n, logits.device)
+    _check_rows(logits, sampled_ids, temperature, top_p)
+    if offsets.dtype != torch.int32 or not offsets.is_cuda or offsets.dim() != 1 or not offsets.is_contiguous():
+        raise ValueError("offsets must be a contiguous 1-D int32 CUDA tensor")
+    if out is not None and (out.dtype != torch.float32 or tuple(out.shape) != (n, 4) or not out.is_contiguous()
+                            or out.device != logits.device):
+        raise ValueError(f"out must be a contiguous float32 [{n}, 4] tensor on {logits.device}")
+    X = torch.empty(n, 4, dtype=torch.float32, device=logits.device) if out is None else out
+    feats = _alloc_features(n, logits.device) if features else None
+    fs = C.byref(_features_struct(feats)) if feats is not None else None
+    st = _abi.lib().pr_feature_sequence(_ptr(logits), _dtype_code(logits), n, V, logits.stride(0),
+                                        _ptr(sampled_ids), _ptr(temperature), _ptr(top_p), _ptr(offsets),
+                                        offsets.shape[0] - 1, int(top_k), _ptr(X), fs, _stream_handle())
+    _abi.check("pr_feature_sequence", st)
+    return (X, feats) if features else X
 
 
 def _params(q=0.1, weights=None, bias=0.0, link="identity") -> _abi.AggParams:

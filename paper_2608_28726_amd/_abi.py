@@ -22,8 +22,10 @@ AGG_FIELDS = ("count", "mean", "min", "quant", "score")
 EXPORTED = (
     "pr_status_string", "pr_agg_params_default", "pr_token_features_workspace", "pr_token_features",
     "pr_request_aggregate", "pr_route", "pr_validate_offsets", "pr_stream_create", "pr_stream_step",
-    "pr_stream_finish", "pr_stream_reset_slots", "pr_stream_destroy",
+    "pr_stream_finish", "pr_stream_reset_slots", "pr_stream_destroy", "pr_feature_sequence",
 )
+
+PR_MAX_TOP_K = 32
 
 
 class TokenFeatures(C.Structure):
@@ -66,6 +68,9 @@ def lib() -> C.CDLL:
     L.pr_token_features_workspace.restype = sz
     L.pr_token_features.argtypes = [vp, C.c_int, i64, i32, i64, vp, vp, vp, C.POINTER(TokenFeatures), vp, sz, vp]
     L.pr_token_features.restype = C.c_int
+    L.pr_feature_sequence.argtypes = [vp, C.c_int, i64, i32, i64, vp, vp, vp, vp, i32, i32, vp,
+                                      C.POINTER(TokenFeatures), vp]
+    L.pr_feature_sequence.restype = C.c_int
     L.pr_request_aggregate.argtypes = [C.POINTER(TokenFeatures), vp, i32, C.POINTER(AggParams),
                                        C.POINTER(RequestAgg), vp]
     L.pr_request_aggregate.restype = C.c_int

@@ -121,6 +121,34 @@ pr_status pr_token_features(const void* logits, pr_dtype dtype, int64_t n_rows, 
   return hip_status(launch_row_features(a, dtype, as_stream(stream)));
 }
 
+pr_status pr_feature_sequence(const void* logits, pr_dtype dtype, int64_t n_rows, int32_t vocab,
+                              int64_t row_stride, const int32_t* sampled_ids, const float* temperature,
+                              const float* top_p, const int32_t* offsets, int32_t n_req, int32_t top_k,
+                              float* X, const pr_token_features_t* features, void* stream) {
+  pr_status st = check_rows(logits, dtype, n_rows, vocab, row_stride, sampled_ids, temperature);
+  if (st != PR_OK) return st;
+  if (top_k < 1 || top_k > PR_MAX_TOP_K || n_req < 0) return PR_ERR_INVALID_ARG;
+  if (features && !features_complete(features)) return PR_ERR_INVALID_ARG;
+  if (n_rows == 0) return PR_OK;
+  if (n_req == 0 || !offsets || !X || !aligned(X, 16)) return PR_ERR_INVALID_ARG;
+  RowArgs a{};
+  a.logits = logits;
+  a.n_rows = n_rows;
+  a.V = vocab;
+  a.row_stride = row_stride;
+  a.sampled_ids = sampled_ids;
+  a.temperature = temperature;
+  a.top_p = top_p;
+  if (features) a.out = *features;
+  a.G = 1;
+  a.X = X;
+  a.offsets = offsets;
+  a.n_req = n_req;
+  a.top_k = top_k;
+  if (top_p) return hip_status(launch_topp(a, dtype, nullptr, as_stream(stream)));
+  return hip_status(launch_feature_sequence(a, dtype, as_stream(stream)));
+}
+
 pr_status pr_request_aggregate(const pr_token_features_t* feats, const int32_t* offsets, int32_t n_req,
                                const pr_agg_params* params, const pr_request_agg_t* out, void* stream) {
   if (n_req < 0 || !out) return PR_ERR_INVALID_ARG;

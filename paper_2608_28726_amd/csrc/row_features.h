@@ -29,6 +29,11 @@ struct RowArgs {
   Partial* ws;              // [n_rows][G] partial states when G > 1
   const int32_t* slot_ids;  // streaming only (NULL offline)
   StreamDev st;             // streaming only
+  // The paper's verifier input sequence (NULL X: not computed).
+  float* X;                 // [n_rows][4]: (l, m, h, rho)
+  const int32_t* offsets;   // [n_req + 1] request boundaries
+  int32_t n_req;
+  int32_t top_k;            // K of the top-K entropy, 1..topk::kMaxK
 };
 
 // Workgroups per row chosen for a shape (the same in every call, so that the
@@ -38,5 +43,9 @@ int row_split(int64_t n_rows, int32_t V, pr_dtype dtype);
 // One kernel when G == 1, partial-state and merge kernels otherwise; with
 // slot ids (streaming) each finalised row also updates its request slot.
 hipError_t launch_row_features(const RowArgs& a, pr_dtype dtype, hipStream_t stream);
+
+// The verifier input sequence X (with the features when a.out is set): one
+// workgroup per row, no split.
+hipError_t launch_feature_sequence(const RowArgs& a, pr_dtype dtype, hipStream_t stream);
 
 }  // namespace pr

@@ -13,7 +13,10 @@
 // shuffles, waves through LDS; a row split over G workgroups merges the G
 // partial states in a second kernel, which also updates the streaming
 // decode state.
+#include <type_traits>
+
 #include "row_scan.h"
+#include "topk.h"
 
 namespace pr {
 
@@ -31,10 +34,13 @@ using namespace scan;
 // SPLIT == true: G workgroups per row write partial states to a.ws; the
 // merge kernel below finalises. Kernel boundaries make the partials visible,
 // so no workgroup waits or fences on another.
-template <typename Tin, int BLOCK, int U, int LD, bool SPLIT>
+// SEQ == true (one workgroup per row): the row's K largest logits are found
+// in the same pass and row r of the verifier input sequence X is written.
+template <typename Tin, int BLOCK, int U, int LD, bool SPLIT, bool SEQ = false>
 __global__ __launch_bounds__(BLOCK)
 __attribute__((amdgpu_waves_per_eu(BLOCK >= 512 ? BLOCK / 256 : PR_ROW_WAVES_PER_EU)))
 void row_features_kernel(RowArgs a) {
+  static_assert(!(SPLIT && SEQ), "the sequence variant keeps a row in one workgroup");
   const int G = a.G;
   const int64_t r = blockIdx.x / G;
   const int g = blockIdx.x % G;
@@ -57,15 +63,32 @@ void row_features_kernel(RowArgs a) {
 
   Lane L;
   lane_init(L);
+  typename std::conditional<SEQ, topk::Hook, NoHook>::type hook;
+  if constexpr (SEQ) hook.init();
   // Workgroups of 512 or more threads run one per CU: there the bucket of
   // each lane's maximum is kept in registers rather than read back at the end.
-  scan_stretch<Tin, BLOCK, U, LD, (BLOCK >= 512)>(row, a.V, vb, ve, g == 0, g == G - 1, nvec, cx, L, v);
+  scan_stretch<Tin, BLOCK, U, LD, (BLOCK >= 512)>(row, a.V, vb, ve, g == 0, g == G - 1, nvec, cx, L, v, hook);
   const Partial p = block_merge<BLOCK>(L, cx.c);
   if (SPLIT) {
     if (threadIdx.x == 0) a.ws[r * G + g] = p;
     return;
   }
   const uint32_t fix = rank_fixup<Tin, BLOCK>(row, a.V, nvec, cx);
+  if constexpr (SEQ) {
+    __shared__ topk::Store<BLOCK> ts;
+    const topk::Lds lds = ts.view();
+    topk::select_topk<Tin, BLOCK, U>(row, a.V, cx.h, vb, ve, nvec, a.top_k, hook, lds);
+    if (threadIdx.x < kWave) {  // the merged state p is valid in the first wave
+      const float H = topk::topk_entropy_f32(lds.top, a.top_k, p.m, cx.c, p.S);
+      const float rho = topk::position_fraction(a.offsets, a.n_req, r);
+      if (threadIdx.x == 0) {
+        float conf[4];
+        const uint32_t flags = finalize_row(a, r, p, cx, fix, conf);
+        write_sequence_row(a, r, conf, flags, H, rho);
+      }
+    }
+    return;
+  }
   if (threadIdx.x == 0) {
     float conf[4];
     finalize_row(a, r, p, cx, fix, conf);
@@ -197,6 +220,29 @@ static hipError_t launch_typed(const RowArgs& a, hipStream_t stream) {
 hipError_t launch_row_features(const RowArgs& a, pr_dtype dtype, hipStream_t stream) {
   if (a.n_rows == 0) return hipSuccess;
   return dtype == PR_BF16 ? launch_typed<uint16_t>(a, stream) : launch_typed<float>(a, stream);
+}
+
+// The sequence variant: the tiers of launch_typed, with one workgroup per row
+// at every batch size.
+template <typename Tin>
+static hipError_t launch_sequence_typed(const RowArgs& a, hipStream_t stream) {
+  constexpr int U = unroll_for<Tin>();
+  constexpr int LD = load_depth_for<Tin>();
+  constexpr int LDW = Elem<Tin>::kVec == 8 ? PR_WIDE_LOAD_DEPTH_BF16 : PR_WIDE_LOAD_DEPTH_F32;
+  const dim3 grid(static_cast<unsigned>(a.n_rows));
+  if (a.n_rows >= kWideRows) {
+    row_features_kernel<Tin, kBlock, U, LD, false, true><<<grid, kBlock, 0, stream>>>(a);
+  } else if (a.n_rows > 256) {
+    row_features_kernel<Tin, kMidBlock, U, LDW, false, true><<<grid, kMidBlock, 0, stream>>>(a);
+  } else {
+    row_features_kernel<Tin, kWideBlock, U, LDW, false, true><<<grid, kWideBlock, 0, stream>>>(a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_feature_sequence(const RowArgs& a, pr_dtype dtype, hipStream_t stream) {
+  if (a.n_rows == 0) return hipSuccess;
+  return dtype == PR_BF16 ? launch_sequence_typed<uint16_t>(a, stream) : launch_sequence_typed<float>(a, stream);
 }
 
 }  // namespace pr

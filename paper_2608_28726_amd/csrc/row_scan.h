@@ -56,13 +56,39 @@ __device__ __forceinline__ void lane_rescale(Lane& L, float m_new, float c) {
   L.a = a_new;
 }
 
-// Per-element hook of the scan: called once per step with the step's logits
-// z and their 2^x (relative to the lane reference L.a, after any rescale),
-// and once per scalar head/tail logit. The row kernel uses none.
+// Per-element hook of the scan: step() is called once per step with the
+// step's logits z, their 2^x (relative to the lane reference L.a, after any
+// rescale), the step's largest logit and its first vector index, before the
+// lane's top-2 bucket maxima take the step in; scalar() likewise once per
+// scalar head/tail logit with its element index; finish() once at the end
+// of the stretch, before the bucket of the lane's maximum is examined. The
+// feature kernel uses none.
 struct NoHook {
   template <int N>
-  __device__ __forceinline__ void step(const float (&)[N], const float (&)[N], float, const Lane&) {}
-  __device__ __forceinline__ void scalar(float, float, const Lane&) {}
+  __device__ __forceinline__ void step(const float (&)[N], const float (&)[N], float, int64_t, const Lane&) {}
+  __device__ __forceinline__ void scalar(float, float, int64_t, const Lane&) {}
+  __device__ __forceinline__ void finish(const Lane&) {}
+};
+
+// Two hooks run side by side.
+template <typename A, typename B>
+struct HookPair {
+  A a;
+  B b;
+  template <int N>
+  __device__ __forceinline__ void step(const float (&z)[N], const float (&e)[N], float cmax, int64_t i,
+                                       const Lane& L) {
+    a.step(z, e, cmax, i, L);
+    b.step(z, e, cmax, i, L);
+  }
+  __device__ __forceinline__ void scalar(float z, float e, int64_t idx, const Lane& L) {
+    a.scalar(z, e, idx, L);
+    b.scalar(z, e, idx, L);
+  }
+  __device__ __forceinline__ void finish(const Lane& L) {
+    a.finish(L);
+    b.finish(L);
+  }
 };
 
 // NV vectors of one lane; vector u has vector index i + u * BLOCK. Every lane
@@ -103,7 +129,7 @@ __device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx&
     L.E0 = fmaf(e0, fmaxf(x0, -kBig), L.E0);
     L.E1 = fmaf(e1, fmaxf(x1, -kBig), L.E1);
   }
-  hook.step(z, ev, cmax, L);
+  hook.step(z, ev, cmax, i, L);
 
   // Rank of y: a vector wholly before y counts z >= z_y (z > next_below(z_y)),
   // any other vector counts z > z_y; ties before y inside y's own vector are
@@ -140,6 +166,13 @@ __device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx&
 template <typename Hook = NoHook>
 __device__ __forceinline__ void consume_scalar(float z, int64_t idx, const RowCtx& cx, Lane& L, Hook& hook) {
   if (z > L.mw) lane_rescale(L, z, cx.c);
+  if (cx.y >= 0) L.cnt += (z > cx.zy || (z == cx.zy && idx < cx.y)) ? 1u : 0u;
+  const float x = fmaf(z, cx.c, -L.a);
+  const float e = fast_exp2(x);
+  L.S0 += e;
+  L.E0 = fmaf(e, fmaxf(x, -kBig), L.E0);
+  hook.scalar(z, e, idx, L);
+  // A scalar logit is a bucket of its own (t1v = -1: t1i is exact).
   if (z > L.t1) {
     L.t2 = L.t1;
     L.t1 = z;
@@ -148,12 +181,6 @@ __device__ __forceinline__ void consume_scalar(float z, int64_t idx, const RowCt
   } else if (z > L.t2) {
     L.t2 = z;
   }
-  if (cx.y >= 0) L.cnt += (z > cx.zy || (z == cx.zy && idx < cx.y)) ? 1u : 0u;
-  const float x = fmaf(z, cx.c, -L.a);
-  const float e = fast_exp2(x);
-  L.S0 += e;
-  L.E0 = fmaf(e, fmaxf(x, -kBig), L.E0);
-  hook.scalar(z, e, L);
 }
 
 // Block-wide merge of the lanes into one Partial (valid in thread 0). Each
@@ -410,6 +437,7 @@ __device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve,
     const int64_t tail0 = cx.h + nvec * VEC;
     for (int64_t e = tail0 + t; e < V; e += BLOCK) consume_scalar(Elem<Tin>::load1(row, e), e, cx, L, hook);
   }
+  hook.finish(L);
   // The lanes holding the wave maximum examine the bucket where their t1 was
   // set (kept in registers, or re-read: a few bytes per wave): its first
   // occurrence gives the exact index (ties across lanes and waves resolve by
@@ -490,9 +518,10 @@ __device__ __forceinline__ uint32_t row_flags(const RowArgs& a, int64_t r, const
 
 // Turns a row's merged state into the outputs (thread 0 writes). With a
 // nucleus, the distribution features are those of the renormalised nucleus.
-// Returns the confidence tuple A = (logprob, maxprob, -entropy, margin).
-__device__ void finalize_row(const RowArgs& a, int64_t r, const Partial& p, const RowCtx& cx, uint32_t fix,
-                             float* conf, const Nucleus* nuc = nullptr) {
+// Fills the confidence tuple A = (logprob, maxprob, -entropy, margin) and
+// returns the row's flags.
+__device__ uint32_t finalize_row(const RowArgs& a, int64_t r, const Partial& p, const RowCtx& cx, uint32_t fix,
+                                 float* conf, const Nucleus* nuc = nullptr) {
   const float T = cx.T;
   uint32_t flags = row_flags(a, r, p, T);
   const float qnan = __uint_as_float(0x7fc00000u);
@@ -555,6 +584,21 @@ __device__ void finalize_row(const RowArgs& a, int64_t r, const Partial& p, cons
     a.out.cutoff[r] = cutoff;
     a.out.flags[r] = flags;
   }
+  return flags;
+}
+
+// Writes row r of the verifier input sequence X: (l, m, h, rho) =
+// (logprob, maxprob, -H^{top-K}, t / T) (Sec. 3.1, Eq. 3). A row whose
+// distribution is undefined (non-finite logits, bad temperature or top-p)
+// gets NaN in l, m and h; rho does not depend on the logits.
+__device__ __forceinline__ void write_sequence_row(const RowArgs& a, int64_t r, const float* conf, uint32_t flags,
+                                                   float H, float rho) {
+  const bool undefined = (flags & (PR_FLAG_NONFINITE | PR_FLAG_BAD_TP)) != 0;
+  float* x = a.X + r * 4;
+  x[0] = conf[0];
+  x[1] = conf[1];
+  x[2] = undefined ? __uint_as_float(0x7fc00000u) : -H;
+  x[3] = rho;
 }
 
 // Streaming: a request slot's running state, read when the row starts (a

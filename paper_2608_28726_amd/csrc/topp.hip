@@ -35,7 +35,10 @@
 // boundary value) that resolves ties by counting.
 #include "topp.h"
 
+#include <type_traits>
+
 #include "row_scan.h"
+#include "topk.h"
 
 namespace pr {
 
@@ -74,6 +77,7 @@ struct TpShared {
   double red_d[2][kNW];
   uint32_t red_u[kNW];
   float red_f[kNW];
+  float topk[topk::kMaxK];  // the row's K largest logits (sequence variant)
   double S64, target, massAbove, Eabove, SN, EN;
   uint32_t b_lo, b_hi, wcount, cntAbove, jfirst, rcount, n_above;
   int32_t hb_lo, hb_hi;
@@ -222,7 +226,7 @@ struct HistHook {
     atomicAdd(&off[idx], static_cast<int32_t>(delta * kOffQ));
   }
   template <int N>
-  __device__ __forceinline__ void step(const float (&z)[N], const float (&)[N], float cmax, const Lane&) {
+  __device__ __forceinline__ void step(const float (&z)[N], const float (&)[N], float cmax, int64_t, const Lane&) {
 #pragma unroll
     for (int k = 0; k < N; ++k) count(z[k]);
     if (__any(fmaf(cmax, kz, k0) < 0.0f)) {  // bf is non-increasing in z
@@ -230,10 +234,11 @@ struct HistHook {
       for (int k = 0; k < N; ++k) add_above(z[k]);
     }
   }
-  __device__ __forceinline__ void scalar(float z, float, const Lane&) {
+  __device__ __forceinline__ void scalar(float z, float, int64_t, const Lane&) {
     count(z);
     add_above(z);
   }
+  __device__ __forceinline__ void finish(const Lane&) {}
   __device__ __forceinline__ void add_above(float z) {
     if (fmaf(z, kz, k0) < 0.0f) {
       const uint32_t slot = atomicAdd(n_above, 1u);
@@ -684,7 +689,29 @@ __device__ bool hist_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec
 
 }  // namespace
 
-template <typename Tin>
+// LDS of the top-K selection, inside the window buffer (unused until the
+// nucleus is computed) except for the result.
+__device__ __forceinline__ topk::Lds topk_lds(TpShared& sh) {
+  static_assert(2144 <= kCap, "top-K scratch fits in the window buffer");
+  float* w = sh.win;
+  topk::Lds s;
+  s.key = reinterpret_cast<uint32_t*>(w);                // 1024 keys
+  s.tag = reinterpret_cast<uint16_t*>(w + 1024);         // 1024 tags
+  s.hist = reinterpret_cast<uint32_t*>(w + 1536);        // 512
+  s.small_key = reinterpret_cast<uint32_t*>(w + 2048);   // 32
+  s.small_tag = reinterpret_cast<uint16_t*>(w + 2080);   // 32
+  s.misc = reinterpret_cast<uint32_t*>(w + 2112);        // 8
+  s.red = reinterpret_cast<uint32_t*>(w + 2120);         // 8
+  s.fail = reinterpret_cast<uint64_t*>(w + 2128);        // 8
+  s.top = sh.topk;
+  s.cap = 1024;
+  return s;
+}
+
+// SEQ: also the row's K largest logits (found in the stats pass) and row r
+// of the verifier input sequence X, with the top-K probabilities taken on the
+// renormalised nucleus.
+template <typename Tin, bool SEQ>
 __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) void topp_kernel(RowArgs a) {
   __shared__ TpShared sh;
   const int64_t r = blockIdx.x;
@@ -721,7 +748,9 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
   for (int k = 1; k < kNW; ++k) A0 = fmaxf(A0, sh.red_f[k]);
   const bool anchored = A0 > -INFINITY && A0 < INFINITY && temperature_ok(cx.T);
   const float invT = 1.0f / cx.T;
-  HistHook hk;
+  HookPair<HistHook, typename std::conditional<SEQ, topk::Hook, NoHook>::type> hp;
+  HistHook& hk = hp.a;
+  if constexpr (SEQ) hp.b.init();
   hk.cnt = sh.u.hs.cnt;
   hk.off = sh.u.hs.off;
   hk.above = sh.above;
@@ -732,9 +761,13 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
   // 1. stats pass, building the histogram
   Lane L;
   lane_init(L);
-  scan_stretch<Tin, kTpBlock, 2, kLD, false>(row, a.V, 0, nvec, true, true, nvec, cx, L, v, hk);
+  scan_stretch<Tin, kTpBlock, 2, kLD, false>(row, a.V, 0, nvec, true, true, nvec, cx, L, v, hp);
   Partial p = block_merge<kTpBlock>(L, cx.c);
   const uint32_t fix = rank_fixup<Tin, kTpBlock>(row, a.V, nvec, cx);
+  if constexpr (SEQ) {
+    topk::select_topk<Tin, kTpBlock, 2>(row, a.V, cx.h, 0, nvec, nvec, a.top_k, hp.b, topk_lds(sh));
+    // the selection's scratch (the window buffer) is free again
+  }
   if (threadIdx.x == 0) {
     sh.p = p;
     sh.fix = fix;
@@ -744,6 +777,18 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
   __syncthreads();
   p = sh.p;
   if (!sh.active) {
+    if constexpr (SEQ) {
+      if (threadIdx.x < kWave) {
+        const float H = topk::topk_entropy_f32(sh.topk, a.top_k, p.m, cx.c, p.S);
+        const float rho = topk::position_fraction(a.offsets, a.n_req, r);
+        if (threadIdx.x == 0) {
+          float conf[4];
+          const uint32_t flags = finalize_row(a, r, p, cx, fix, conf);
+          write_sequence_row(a, r, conf, flags, H, rho);
+        }
+      }
+      return;
+    }
     if (threadIdx.x == 0) {
       float conf[4];
       finalize_row(a, r, p, cx, fix, conf);
@@ -760,6 +805,19 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
   Nucleus nuc;
   if (!(anchored && hist_nucleus<Tin>(row, a.V, cx.h, nvec, D, P, A0, hk, sh, nuc)))
     nuc = legacy_nucleus<Tin>(row, a.V, cx.h, nvec, D, P, sh);
+  if constexpr (SEQ) {
+    if (threadIdx.x < kWave) {
+      const int j = a.top_k < nuc.k ? a.top_k : nuc.k;  // the nucleus may hold fewer than K tokens
+      const float H = topk::topk_entropy_f64(sh.topk, j, p.m, T, nuc.S);
+      const float rho = topk::position_fraction(a.offsets, a.n_req, r);
+      if (threadIdx.x == 0) {
+        float conf[4];
+        const uint32_t flags = finalize_row(a, r, p, cx, fix, conf, &nuc);
+        write_sequence_row(a, r, conf, flags, H, rho);
+      }
+    }
+    return;
+  }
   if (threadIdx.x == 0) {
     float conf[4];
     finalize_row(a, r, p, cx, fix, conf, &nuc);
@@ -771,10 +829,18 @@ size_t topp_workspace(pr_dtype, int64_t, int32_t) { return 0; }
 hipError_t launch_topp(const RowArgs& a, pr_dtype dtype, void*, hipStream_t stream) {
   if (a.n_rows == 0) return hipSuccess;
   const dim3 grid(static_cast<unsigned>(a.n_rows));
-  if (dtype == PR_BF16)
-    topp_kernel<uint16_t><<<grid, kTpBlock, 0, stream>>>(a);
-  else
-    topp_kernel<float><<<grid, kTpBlock, 0, stream>>>(a);
+  const bool seq = a.X != nullptr;
+  if (dtype == PR_BF16) {
+    if (seq)
+      topp_kernel<uint16_t, true><<<grid, kTpBlock, 0, stream>>>(a);
+    else
+      topp_kernel<uint16_t, false><<<grid, kTpBlock, 0, stream>>>(a);
+  } else {
+    if (seq)
+      topp_kernel<float, true><<<grid, kTpBlock, 0, stream>>>(a);
+    else
+      topp_kernel<float, false><<<grid, kTpBlock, 0, stream>>>(a);
+  }
   return hipGetLastError();
 }
 

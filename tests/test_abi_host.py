@@ -106,3 +106,42 @@ def test_other_entry_points_reject_bad_arguments():
     feats = _abi.TokenFeatures(*([8] * 10))
     assert lib.pr_token_features(None, 0, 0, 100, 100, None, None, None, C.byref(feats), None, 0, None) == \
         _abi.PR_OK
+
+
+@pytest.mark.parametrize("case", ["k=0", "k>max", "null offsets", "no requests", "null X", "misaligned X",
+                                  "partial features", "V<2", "n_req<0"])
+def test_feature_sequence_rejects_bad_arguments(case):
+    lib = ensure_built()
+    from paper_2608_28726_amd import _abi
+    args = dict(logits=C.c_void_p(64), dtype=1, n=4, V=100, stride=100, ids=C.c_void_p(64),
+                temps=C.c_void_p(64), offsets=C.c_void_p(64), n_req=2, k=20, X=C.c_void_p(256), feats=None)
+    if case == "k=0":
+        args["k"] = 0
+    elif case == "k>max":
+        args["k"] = _abi.PR_MAX_TOP_K + 1
+    elif case == "null offsets":
+        args["offsets"] = None
+    elif case == "no requests":
+        args["n_req"] = 0
+    elif case == "null X":
+        args["X"] = None
+    elif case == "misaligned X":
+        args["X"] = C.c_void_p(260)
+    elif case == "partial features":
+        f = _abi.TokenFeatures(*([8] * 9 + [None]))
+        args["feats"] = C.byref(f)
+    elif case == "V<2":
+        args["V"], args["stride"] = 1, 1
+    elif case == "n_req<0":
+        args["n_req"] = -1
+    st = lib.pr_feature_sequence(args["logits"], args["dtype"], args["n"], args["V"], args["stride"], args["ids"],
+                                 args["temps"], None, args["offsets"], args["n_req"], args["k"], args["X"],
+                                 args["feats"], None)
+    assert st == _abi.PR_ERR_INVALID_ARG
+
+
+def test_feature_sequence_zero_rows_is_valid():
+    lib = ensure_built()
+    from paper_2608_28726_amd import _abi
+    assert lib.pr_feature_sequence(None, 1, 0, 100, 100, None, None, None, None, 0, 20, None, None, None) == \
+        _abi.PR_OK
