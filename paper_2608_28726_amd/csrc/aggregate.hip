@@ -291,16 +291,26 @@ __global__ __launch_bounds__(kAggBlock) void stream_finish_kernel(StreamDev s, c
   const int64_t cnt = ok ? s.count[slot] : 0;
   const bool kept = cnt <= s.max_len;
   const int w = threadIdx.x / kWave;
+  // The slot's running sums, minima and NaN bits are read before the
+  // quantile select, so that their latency overlaps the history's.
+  double sum = 0.0;
+  float mn = 0.0f;
+  uint32_t nanb = 0;
+  if (cnt > 0) {
+    sum = s.sum[slot * 4 + w];
+    mn = s.minv[slot * 4 + w];
+    nanb = s.nanbits[slot];
+  }
   float q = __uint_as_float(0x7fc00000u);
   if (cnt > 0 && kept) {
     const HistCol get{s.hist + (static_cast<int64_t>(slot) * 4 + w) * s.max_len};
     q = radix_select(get, 0, cnt, quant_rank(hp.q, cnt), sh.hist, sh.sel);
   }
   if (threadIdx.x % kWave == 0) {
-    sh.mean_d[w] = cnt > 0 ? s.sum[slot * 4 + w] / static_cast<double>(cnt) : 0.0;
-    sh.mn[w] = cnt > 0 ? s.minv[slot * 4 + w] : 0.0f;
+    sh.mean_d[w] = cnt > 0 ? sum / static_cast<double>(cnt) : 0.0;
+    sh.mn[w] = mn;
     sh.qu[w] = q;
-    sh.nan[w] = (cnt > 0 && ((s.nanbits[slot] >> w) & 1u)) ? 1u : 0u;
+    sh.nan[w] = ((nanb >> w) & 1u) ? 1u : 0u;
   }
   __syncthreads();
   if (threadIdx.x == 0) {

@@ -12,7 +12,7 @@ struct pr_stream {
   int device;
   StreamDev dev;
   pr_agg_params params;
-  Partial* ws;  // [max_slots][kStreamMaxSplit]
+  Partial* ws;  // split-row workspace for up to max_slots rows of kStreamMaxSplit workgroups
   void* block;  // single allocation backing everything above
 };
 
@@ -92,8 +92,7 @@ void pr_agg_params_default(pr_agg_params* params) {
 size_t pr_token_features_workspace(pr_dtype dtype, int64_t n_rows, int32_t vocab, int32_t top_p_on) {
   if (n_rows <= 0 || vocab < 2) return 0;
   if (top_p_on) return topp_workspace(dtype, n_rows, vocab);
-  const int G = row_split(n_rows, vocab, dtype);
-  return G > 1 ? static_cast<size_t>(n_rows) * G * sizeof(Partial) : 0;
+  return split_workspace_bytes(n_rows, row_split(n_rows, vocab, dtype));
 }
 
 pr_status pr_token_features(const void* logits, pr_dtype dtype, int64_t n_rows, int32_t vocab,
@@ -193,7 +192,7 @@ pr_status pr_stream_create(int32_t max_slots, int32_t max_len, const pr_agg_para
   const size_t S = static_cast<size_t>(max_slots);
   const size_t L = static_cast<size_t>(max_len);
   auto up = [](size_t b) { return (b + 255) & ~size_t{255}; };
-  const size_t b_ws = up(S * kStreamMaxSplit * sizeof(Partial));
+  const size_t b_ws = up(split_workspace_bytes(static_cast<int64_t>(S), kStreamMaxSplit));
   const size_t b_sum = up(S * 4 * sizeof(double));
   const size_t b_hist = up(S * 4 * L * sizeof(float));
   const size_t b_min = up(S * 4 * sizeof(float));

@@ -16,6 +16,15 @@ struct StreamDev {
   float* hist;        // [max_slots][4][max_len] every token's A, for the exact quantile
 };
 
+// What the merge of a split row needs from the row besides the partial
+// states: written by the row's first workgroup.
+struct RowMeta {
+  float T;       // temperature
+  float zy;      // logit of the sampled token (NaN when the id is invalid)
+  int32_t y;     // sampled id, -1 when invalid
+  uint32_t fix;  // rank corrections the vector loop leaves out
+};
+
 struct RowArgs {
   const void* logits;
   int64_t n_rows;
@@ -26,7 +35,7 @@ struct RowArgs {
   const float* top_p;
   pr_token_features_t out;  // max_logit == NULL: outputs not written (streaming only)
   int G;                    // workgroups per row
-  Partial* ws;              // [n_rows][G] partial states when G > 1
+  Partial* ws;              // [n_rows][G] partial states when G > 1, then RowMeta [n_rows]
   const int32_t* slot_ids;  // streaming only (NULL offline)
   StreamDev st;             // streaming only
   // The paper's verifier input sequence (NULL X: not computed).
@@ -39,6 +48,16 @@ struct RowArgs {
 // Workgroups per row chosen for a shape (the same in every call, so that the
 // workspace size query and the launch agree).
 int row_split(int64_t n_rows, int32_t V, pr_dtype dtype);
+
+// Bytes of split-row workspace for n_rows rows of G workgroups each.
+inline size_t split_workspace_bytes(int64_t n_rows, int G) {
+  return G > 1 ? static_cast<size_t>(n_rows) * (static_cast<size_t>(G) * sizeof(Partial) + sizeof(RowMeta)) : 0;
+}
+
+// The RowMeta records after the partial states.
+__host__ __device__ inline RowMeta* split_meta(Partial* ws, int64_t n_rows, int G) {
+  return reinterpret_cast<RowMeta*>(ws + n_rows * G);
+}
 
 // One kernel when G == 1, partial-state and merge kernels otherwise; with
 // slot ids (streaming) each finalised row also updates its request slot.

@@ -71,6 +71,10 @@ void row_features_kernel(RowArgs a) {
   const Partial p = block_merge<BLOCK>(L, cx.c);
   if (SPLIT) {
     if (threadIdx.x == 0) a.ws[r * G + g] = p;
+    if (g == 0) {  // the row's context and rank corrections for the merge
+      const uint32_t fix = rank_fixup<Tin, BLOCK>(row, a.V, nvec, cx);
+      if (threadIdx.x == 0) split_meta(a.ws, a.n_rows, G)[r] = RowMeta{cx.T, cx.zy, cx.y, fix};
+    }
     return;
   }
   const uint32_t fix = rank_fixup<Tin, BLOCK>(row, a.V, nvec, cx);
@@ -96,21 +100,53 @@ void row_features_kernel(RowArgs a) {
   }
 }
 
-// Merges each row's G partials in index order and finalises the row.
-template <typename Tin, int BLOCK>
-__global__ __launch_bounds__(BLOCK) void row_merge_kernel(RowArgs a) {
+// Merges each row's G partial states and finalises the row: one wave per
+// row, lane g holding partial g (G <= 64). Every input (the partials, the
+// row's context record and the slot state) is loaded at once, so the merge
+// costs one memory round trip.
+__global__ __launch_bounds__(kWave) void row_merge_kernel(RowArgs a) {
   const int64_t r = blockIdx.x;
   if (r >= a.n_rows) return;
-  constexpr int VEC = Elem<Tin>::kVec;
-  const void* row = static_cast<const Tin*>(a.logits) + r * a.row_stride;
-  const RowCtx cx = row_ctx<Tin>(a, r, row);
-  const int64_t nvec = (a.V - cx.h) / VEC;
+  const int G = a.G;
+  const int lane = threadIdx.x;
+  Partial q;
+  if (lane < G) {
+    q = a.ws[r * G + lane];
+  } else {
+    q.m = -INFINITY;
+    q.S = 0.0f;
+    q.E = 0.0f;
+    q.t1 = -INFINITY;
+    q.t1i = kNoIndex;
+    q.t2 = -INFINITY;
+    q.cnt = 0;
+    q.pad = 0;
+  }
+  const RowMeta meta = split_meta(a.ws, a.n_rows, G)[r];
   const SlotState ss = slot_load(a, r);
-  const uint32_t fix = rank_fixup<Tin, BLOCK>(row, a.V, nvec, cx);
-  if (threadIdx.x == 0) {
-    const Partial p = merge_partials(a.ws + r * a.G, a.G, cx.c);
+  RowCtx cx;
+  cx.T = meta.T;
+  cx.c = temperature_ok(meta.T) ? kLog2e / meta.T : kLog2e;
+  cx.zy = meta.zy;
+  cx.y = meta.y;
+  cx.fix_vec = 0;
+  cx.h = 0;
+  cx.thr_before = 0.0f;
+  cx.thr_lo = 0.0f;
+  Partial p;
+  p.m = wave_max(q.m);
+  rebase(q.m == -INFINITY, q.m * cx.c, p.m * cx.c, q.S, q.E);
+  p.S = wave_sum(q.S);
+  p.E = wave_sum(q.E);
+  wave_top2(q.t1, q.t1i, q.t2);
+  p.t1 = q.t1;
+  p.t1i = q.t1i;
+  p.t2 = q.t2;
+  p.cnt = wave_sum_u(q.cnt);
+  p.pad = 0;
+  if (lane == 0) {
     float conf[4];
-    finalize_row(a, r, p, cx, fix, conf);
+    finalize_row(a, r, p, cx, meta.fix, conf);
     stream_update(a.st, ss, conf);
   }
 }
@@ -212,7 +248,7 @@ static hipError_t launch_typed(const RowArgs& a, hipStream_t stream) {
     row_features_kernel<Tin, kWideBlock, U, LDW, false><<<grid, kWideBlock, 0, stream>>>(a);
   } else {
     row_features_kernel<Tin, kSplitBlock, U, LDW, true><<<grid, kSplitBlock, 0, stream>>>(a);
-    row_merge_kernel<Tin, kWave><<<dim3(static_cast<unsigned>(a.n_rows)), kWave, 0, stream>>>(a);
+    row_merge_kernel<<<dim3(static_cast<unsigned>(a.n_rows)), kWave, 0, stream>>>(a);
   }
   return hipGetLastError();
 }

@@ -238,31 +238,6 @@ __device__ Partial block_merge(Lane& L, float c) {
   return p;
 }
 
-// Merge of G per-workgroup partial states of one row, in index order.
-__device__ Partial merge_partials(const Partial* parts, int G, float c) {
-  float M = parts[0].m;
-  for (int g = 1; g < G; ++g) M = fmaxf(M, parts[g].m);
-  const float A = M * c;
-  Partial p;
-  p.m = M;
-  p.S = 0.0f;
-  p.E = 0.0f;
-  p.t1 = -INFINITY;
-  p.t1i = kNoIndex;
-  p.t2 = -INFINITY;
-  p.cnt = 0;
-  p.pad = 0;
-  for (int g = 0; g < G; ++g) {
-    Partial q = parts[g];
-    rebase(q.m == -INFINITY, q.m * c, A, q.S, q.E);
-    p.S += q.S;
-    p.E += q.E;
-    top2_merge(p.t1, p.t1i, p.t2, q.t1, q.t1i, q.t2);
-    p.cnt += q.cnt;
-  }
-  return p;
-}
-
 template <typename Tin>
 __device__ __forceinline__ int64_t head_elems(const void* row, int32_t V) {
   const uintptr_t addr = reinterpret_cast<uintptr_t>(row);
