@@ -14,13 +14,17 @@ ship rule p >= tau):
   over a ragged batch, the summary score and the ship-or-escalate rule.
 * :mod:`oracle.sequence` -- the paper's own verifier input: the top-K
   entropy (K = 20) and the stacked per-token tuples (l, m, h, rho).
+* :mod:`oracle.head` -- the paper's verifier head over that input:
+  projection with positional encoding, two post-norm encoder layers, mean
+  pool and sigmoid (run with seeded synthetic weights).
 
-Parity pinning: every function here is pinned by ``tests/test_oracle_pins.py``
-and ``tests/test_oracle_sequence.py`` against closed forms, invariants and
-pure-Python brute force, except the
-default score head (a fixed linear summary chosen because the paper
-publishes no trained head weights), which is *parity unpinned* against the
-paper.
+Parity pinning: every function here is pinned by ``tests/test_oracle_pins.py``,
+``tests/test_oracle_sequence.py`` and ``tests/test_oracle_head.py`` against
+closed forms, invariants, pure-Python brute force and (for the head) an
+independent implementation of the same architecture, except the default
+score head (a fixed linear summary chosen because the paper publishes no
+trained head weights) and the transformer head's weights, which are *parity
+unpinned* against the paper.
 """
 
 from .features import (  # noqa: F401
@@ -45,3 +49,4 @@ from .sequence import (  # noqa: F401
     topk_entropy,
     topk_entropy_batch,
 )
+from .head import HEAD_WEIGHTS, head_score, head_scores  # noqa: F401,E402

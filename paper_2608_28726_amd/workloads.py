@@ -211,3 +211,33 @@ def to_host_raw(logits: torch.Tensor) -> np.ndarray:
     if t.dtype == torch.bfloat16:
         return t.view(torch.int16).numpy().view(np.uint16)
     return t.numpy()
+
+
+# Parameter tensors of the verifier head in storage order, with the fan-in
+# that scales their synthetic initial values (input recipe only; the layout
+# itself is documented with pr_verifier_head in include/prouter.h).
+_HEAD_TENSORS = (
+    [("W_in", 64 * 4, 4), ("b_in", 64, 4)]
+    + [t for _ in range(2) for t in (
+        ("W_qkv", 192 * 64, 64), ("b_qkv", 192, 64), ("W_o", 64 * 64, 64), ("b_o", 64, 64),
+        ("ln1_g", 64, None), ("ln1_b", 64, None), ("W_1", 128 * 64, 64), ("b_1", 128, 64),
+        ("W_2", 64 * 128, 128), ("b_2", 64, 128), ("ln2_g", 64, None), ("ln2_b", 64, None))]
+    + [("w_out", 64, 64), ("b_out", 1, 64)]
+)
+
+
+def head_weights(seed: int = 0x50524844) -> np.ndarray:
+    """Seeded synthetic weights of the verifier head (the paper publishes
+    none): linear weights and biases ~ U(-1/sqrt(fan_in), 1/sqrt(fan_in)),
+    LayerNorm gains ~ 1 + U(-0.1, 0.1) and shifts ~ U(-0.1, 0.1). Flat
+    float32, 67,329 entries."""
+    rng = np.random.default_rng(seed)
+    parts = []
+    for name, n, fan_in in _HEAD_TENSORS:
+        if fan_in is None:
+            v = rng.uniform(-0.1, 0.1, n) + (1.0 if name.endswith("_g") else 0.0)
+        else:
+            a = 1.0 / np.sqrt(fan_in)
+            v = rng.uniform(-a, a, n)
+        parts.append(v.astype(np.float32))
+    return np.concatenate(parts)
