@@ -33,9 +33,10 @@ def parse_args():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="ragged_64req_v151936_bf16")
-    ap.add_argument("--path", choices=("features", "sequence"), default="features",
+    ap.add_argument("--path", choices=("features", "sequence", "pipeline"), default="features",
                     help="features: per-token features, per-request summaries and route (the default); "
-                         "sequence: the paper's verifier input sequence (l, m, top-20 entropy, t/T) per token")
+                         "sequence: the paper's verifier input sequence (l, m, top-20 entropy, t/T) per token; "
+                         "pipeline: that sequence, the paper's transformer head (synthetic weights) and route")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="time budget of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
@@ -47,6 +48,19 @@ def parse_args():
 
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
+
+
+MFMA_F32_PEAK_TFLOPS = 157.3  # dense float32 matrix/vector peak of the part
+
+
+def head_flops(lengths) -> float:
+    """Floating-point operations of the verifier head over requests of these
+    lengths: per token the 4 -> 64 projection, per layer the QKV, output and
+    feed-forward products and the attention products (QK^T, PV) over the
+    request's tokens."""
+    T = np.asarray(lengths, dtype=np.float64)
+    per_layer = 2 * T * 64 * 192 + 2 * 2 * T * T * 64 + 2 * T * 64 * 64 + 2 * 2 * T * 64 * 128
+    return float(np.sum(2 * T * 4 * 64 + 2 * per_layer))
 
 
 def algorithmic_bytes_per_row(V: int, elem_bytes: int) -> int:
@@ -196,7 +210,13 @@ def run_offline(args, torch, pr, wl, w):
     log(f"[bench] {w.name}: {n_rows} rows in {n_chunks} chunk(s), {copies} rotating copies, "
         f"{n_rows * w.V * w.elem_bytes / 1e9:.2f} GB per step")
     offs = [torch.as_tensor(b.offsets).cuda() for b in batches]
-    sequence = args.path == "sequence"
+    sequence = args.path in ("sequence", "pipeline")
+    pipeline = args.path == "pipeline"
+    if pipeline:
+        head_w = torch.tensor(wl.head_weights(), device="cuda")
+        head_ws = [torch.empty(max(int(pr._abi.lib().pr_verifier_head_workspace(b.n_rows)), 1), dtype=torch.uint8,
+                               device="cuda") for b in batches]
+        head_ev = []
     if sequence:
         feats = [torch.empty(b.n_rows, 4, dtype=torch.float32, device="cuda") for b in batches]
     else:
@@ -223,7 +243,15 @@ def run_offline(args, torch, pr, wl, w):
                                   workspace=wss[c])
             if ev is not None and c == group[-1]:
                 ev[1].record()
-            if not sequence:
+            if pipeline:
+                h0, h1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                h0.record()
+                scores = pr.verifier_head(feats[c], offs[c], head_w, max_len=w.len_hi, workspace=head_ws[c])
+                h1.record()
+                if ev is not None:
+                    head_ev.append((h0, h1))
+                out = pr.route(scores, w.tau)
+            elif not sequence:
                 agg = pr.request_aggregate(feats[c], offs[c], q=w.q)
                 out = pr.route(agg["score"], w.tau)
         return out
@@ -249,6 +277,12 @@ def run_offline(args, torch, pr, wl, w):
     if n_chunks > 1:  # events bracket all chunks' row kernels and their summaries
         kernel += f" x{n_chunks} chunks (+summaries)"
     extra = {"kernel": kernel, "kernel_ms": kern_ms, "bytes_per_launch": bytes_launch}
+    if pipeline:
+        head_ms = float(np.mean([a.elapsed_time(b) for a, b in head_ev]))
+        flops = sum(head_flops(np.diff(b.offsets)) for b in batches) / copies
+        extra["head"] = {"ms": head_ms, "gflop": flops / 1e9, "tflop_per_s": flops / (head_ms * 1e-3) / 1e12,
+                         "peak_tflop_per_s": MFMA_F32_PEAK_TFLOPS, "weights": "synthetic (seeded)"}
+        log(f"[bench] verifier head {head_ms * 1e3:.1f} us per batch, {flops / 1e9:.2f} GFLOP")
     return batches[0], feats[0], n_rows, elapsed, kern_ms, bytes_launch, extra
 
 
@@ -421,8 +455,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "n_req": w.n_req, "rows": n_rows, "V": w.V, "logits": w.dtype,
                    "mode": "streaming decode, one step per token" if stream_mode else "offline ragged batch",
-                   "path": "verifier input sequence (l, m, top-20 entropy, t/T)" if args.path == "sequence"
-                   else "features, summaries, route",
+                   "path": {"sequence": "verifier input sequence (l, m, top-20 entropy, t/T)",
+                            "pipeline": "verifier input sequence, transformer head (synthetic weights), route"}.get(
+                                args.path, "features, summaries, route"),
                    "temperature": [w.T_lo, w.T_hi], "top_p": None if w.P_lo is None else [w.P_lo, w.P_hi],
                    "aggregation": f"mean/min/q={w.q} nearest-rank", "threshold": w.tau},
         "gb_per_s": achieved,
@@ -434,7 +469,7 @@ def main():
         result["copy_probe"] = copy_probe(torch)
     if not args.no_cpu_baseline and batch is not None:
         log("[bench] timing the oracle on the host")
-        if args.path == "sequence":
+        if args.path in ("sequence", "pipeline"):
             result["cpu_baseline"] = cpu_baseline_sequence(torch, batch, feats, args.cpu_seconds, pr.PAPER_TOP_K)
         else:
             result["cpu_baseline"] = cpu_baseline(torch, batch, feats, args.cpu_seconds)

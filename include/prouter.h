@@ -182,6 +182,42 @@ pr_status pr_feature_sequence(const void* logits, pr_dtype dtype, int64_t n_rows
                               const float* top_p, const int32_t* offsets, int32_t n_req, int32_t top_k,
                               float* X, const pr_token_features_t* features, void* stream);
 
+/* The verifier head (Sec. 3.1, the paragraph after Eq. 3; Sec. 4.2): its
+ * number of float32 parameters, and the device workspace it needs. */
+#define PR_HEAD_WEIGHTS 67329
+size_t pr_verifier_head_workspace(int64_t n_rows);
+
+/*
+ * The paper's shipping confidence of each request from its input sequence X
+ * (Sec. 3.1, after Eq. 3): a linear projection of each token's 4 features to
+ * 64 with the sinusoidal positional encoding of its position t - 1 added,
+ * two post-norm transformer encoder layers (4 heads of 16 dimensions,
+ * softmax over every token of the same request, feed-forward width 128 with
+ * ReLU, LayerNorm over the 64 features with eps 1e-5), the mean over the
+ * request's tokens, a linear map to one logit and the logistic sigmoid.
+ * Computed in float32. The paper publishes no weights; any weights of this
+ * shape may be passed.
+ *   X          float [n_rows][4], device (as written by pr_feature_sequence).
+ *   offsets    int32 [n_req + 1], device; precondition as for
+ *              pr_request_aggregate.
+ *   max_len    at least the number of tokens of the longest request; a
+ *              longer request scores NaN (the attention grid is sized by it).
+ *   weights    float [PR_HEAD_WEIGHTS], device, in this order (matrices
+ *              row-major [out][in]): W_in [64][4], b_in [64]; per layer:
+ *              W_qkv [192][64] (query rows, then key rows, then value rows;
+ *              head k owns rows 16k .. 16k+15 of each), b_qkv [192],
+ *              W_o [64][64], b_o [64], LayerNorm-1 gain [64] and shift [64],
+ *              W_1 [128][64], b_1 [128], W_2 [64][128], b_2 [64],
+ *              LayerNorm-2 gain [64] and shift [64]; then w_out [64], b_out [1].
+ *   scores     float [n_req], device. An empty request scores NaN (it
+ *              escalates under pr_route).
+ *   workspace  device scratch of at least pr_verifier_head_workspace(n_rows)
+ *              bytes, 16-byte aligned; no initialisation needed.
+ */
+pr_status pr_verifier_head(const float* X, int64_t n_rows, const int32_t* offsets, int32_t n_req, int32_t max_len,
+                           const float* weights, float* scores, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
 /*
  * Ragged per-request summaries and score (Sec. 3.1, the stacked feature
  * sequence X; Sec. 4.2, Table "ablation", quantile-summary input).

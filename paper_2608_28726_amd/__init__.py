@@ -25,7 +25,7 @@ from . import _abi
 from ._abi import (FLAG_BAD_ID, FLAG_BAD_TP, FLAG_NONFINITE, FLAG_OUTSIDE_NUCLEUS,  # noqa: F401
                    ProuterError)
 
-__all__ = ["token_features", "feature_sequence", "request_aggregate", "route", "validate_offsets", "StreamState",
+__all__ = ["token_features", "feature_sequence", "verifier_head", "request_aggregate", "route", "validate_offsets", "StreamState",
            "token_features_workspace", "ProuterError", "FEATURE_FLOATS", "FEATURE_INTS", "PAPER_TOP_K"]
 
 PAPER_TOP_K = 20  # K of the paper's top-K entropy (Sec. 3.1)
@@ -139,6 +139,34 @@ def feature_sequence(logits: torch.Tensor, sampled_ids: torch.Tensor, temperatur
                                         offsets.shape[0] - 1, int(top_k), _ptr(X), fs, _stream_handle())
     _abi.check("pr_feature_sequence", st)
     return (X, feats) if features else X
+
+
+def verifier_head(X: torch.Tensor, offsets: torch.Tensor, weights: torch.Tensor, max_len: int | None = None,
+                  workspace: torch.Tensor | None = None) -> torch.Tensor:
+    """The paper's shipping confidence per request from its input sequence
+    (``pr_verifier_head``). ``X`` float32 [n_rows, 4] (as returned by
+    :func:`feature_sequence`), ``offsets`` int32 [n_req + 1], ``weights``
+    float32 [67,329] in the documented layout. ``max_len``: at least the
+    longest request's length (default: n_rows). Returns float32 [n_req]."""
+    if X.dtype != torch.float32 or not X.is_cuda or X.dim() != 2 or X.shape[1] != 4 or not X.is_contiguous():
+        raise ValueError("X must be a contiguous float32 [n_rows, 4] CUDA tensor")
+    if offsets.dtype != torch.int32 or not offsets.is_cuda or offsets.dim() != 1 or not offsets.is_contiguous():
+        raise ValueError("offsets must be a contiguous 1-D int32 CUDA tensor")
+    if (weights.dtype != torch.float32 or not weights.is_cuda or weights.numel() != _abi.PR_HEAD_WEIGHTS
+            or not weights.is_contiguous()):
+        raise ValueError(f"weights must be a contiguous float32 CUDA tensor of {_abi.PR_HEAD_WEIGHTS} entries")
+    n = X.shape[0]
+    n_req = offsets.shape[0] - 1
+    L = _abi.lib()
+    need = int(L.pr_verifier_head_workspace(n))
+    if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
+        workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    scores = torch.empty(n_req, dtype=torch.float32, device=X.device)
+    st = L.pr_verifier_head(_ptr(X), n, _ptr(offsets), n_req, int(max_len if max_len is not None else max(n, 1)),
+                            _ptr(weights), _ptr(scores), _ptr(workspace), ws_bytes, _stream_handle())
+    _abi.check("pr_verifier_head", st)
+    return scores
 
 
 def _params(q=0.1, weights=None, bias=0.0, link="identity") -> _abi.AggParams:

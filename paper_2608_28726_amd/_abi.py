@@ -23,7 +23,10 @@ EXPORTED = (
     "pr_status_string", "pr_agg_params_default", "pr_token_features_workspace", "pr_token_features",
     "pr_request_aggregate", "pr_route", "pr_validate_offsets", "pr_stream_create", "pr_stream_step",
     "pr_stream_finish", "pr_stream_reset_slots", "pr_stream_destroy", "pr_feature_sequence",
+    "pr_verifier_head_workspace", "pr_verifier_head",
 )
+
+PR_HEAD_WEIGHTS = 67329
 
 PR_MAX_TOP_K = 32
 
@@ -71,6 +74,10 @@ def lib() -> C.CDLL:
     L.pr_feature_sequence.argtypes = [vp, C.c_int, i64, i32, i64, vp, vp, vp, vp, i32, i32, vp,
                                       C.POINTER(TokenFeatures), vp]
     L.pr_feature_sequence.restype = C.c_int
+    L.pr_verifier_head_workspace.argtypes = [i64]
+    L.pr_verifier_head_workspace.restype = sz
+    L.pr_verifier_head.argtypes = [vp, i64, vp, i32, i32, vp, vp, vp, sz, vp]
+    L.pr_verifier_head.restype = C.c_int
     L.pr_request_aggregate.argtypes = [C.POINTER(TokenFeatures), vp, i32, C.POINTER(AggParams),
                                        C.POINTER(RequestAgg), vp]
     L.pr_request_aggregate.restype = C.c_int

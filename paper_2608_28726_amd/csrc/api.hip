@@ -4,6 +4,7 @@
 #include <new>
 
 #include "aggregate.h"
+#include "head.h"
 #include "topp.h"
 
 using namespace pr;
@@ -146,6 +147,30 @@ pr_status pr_feature_sequence(const void* logits, pr_dtype dtype, int64_t n_rows
   a.top_k = top_k;
   if (top_p) return hip_status(launch_topp(a, dtype, nullptr, as_stream(stream)));
   return hip_status(launch_feature_sequence(a, dtype, as_stream(stream)));
+}
+
+size_t pr_verifier_head_workspace(int64_t n_rows) { return n_rows > 0 ? head_workspace_bytes(n_rows) : 0; }
+
+pr_status pr_verifier_head(const float* X, int64_t n_rows, const int32_t* offsets, int32_t n_req, int32_t max_len,
+                           const float* weights, float* scores, void* workspace, size_t workspace_bytes,
+                           void* stream) {
+  if (n_rows < 0 || n_req < 0 || max_len < 1) return PR_ERR_INVALID_ARG;
+  if (n_rows > (int64_t{1} << 30)) return PR_ERR_UNSUPPORTED;
+  if (n_req == 0) return PR_OK;
+  if (!offsets || !weights || !scores) return PR_ERR_INVALID_ARG;
+  if (n_rows > 0 && (!X || !aligned(X, 4))) return PR_ERR_INVALID_ARG;
+  const size_t need = pr_verifier_head_workspace(n_rows);
+  if (need > 0 && (!workspace || workspace_bytes < need || !aligned(workspace, 16))) return PR_ERR_INVALID_ARG;
+  HeadArgs a{};
+  a.X = X;
+  a.n_rows = n_rows;
+  a.offsets = offsets;
+  a.n_req = n_req;
+  a.max_len = max_len;
+  a.weights = weights;
+  a.scores = scores;
+  a.ws = static_cast<float*>(workspace);
+  return hip_status(launch_head(a, as_stream(stream)));
 }
 
 pr_status pr_request_aggregate(const pr_token_features_t* feats, const int32_t* offsets, int32_t n_req,

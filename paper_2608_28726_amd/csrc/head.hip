@@ -1,0 +1,437 @@
+// The paper's verifier head on the GPU (Pro-Router, Sec. 3.1, the paragraph
+// after Eq. 3; Sec. 4.2): each request's input sequence X (T tokens x 4
+// features) is projected to 64 features with a sinusoidal positional
+// encoding, passes two post-norm transformer encoder layers (4 heads of 16,
+// feed-forward width 128, LayerNorm eps 1e-5), is mean-pooled over its
+// tokens and mapped to one shipping confidence by a linear map and a sigmoid.
+//
+// The tokens of all requests are processed together as rows:
+//  head_qkv_kernel   64-row tiles: (first layer: projection + encoding), the
+//                    QKV projection on MFMA (v_mfma_f32_16x16x4f32);
+//  head_attn_kernel  4 waves per (request, head, 64 queries), splitting the
+//                    request's keys: online softmax per wave, states merged
+//                    through LDS;
+//  head_ffn_kernel   64-row tiles: output projection, residual, LayerNorm,
+//                    feed-forward (MFMA), residual, LayerNorm;
+//  head_pool_kernel  one workgroup per request: mean pool, linear, sigmoid.
+// Everything is float32 with float32 accumulation.
+#include "head.h"
+
+namespace pr {
+
+namespace {
+
+constexpr int D = kHeadD;       // 64
+constexpr int FF = kHeadFF;     // 128
+constexpr int NH = kHeadHeads;  // 4
+constexpr int DH = D / NH;      // 16
+constexpr int QKV = 3 * D;      // 192
+constexpr int kTile = 64;       // rows per tile
+constexpr int kTileThreads = 256;
+constexpr float kLnEps = 1e-5f;
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+// Offsets (floats) of the parameter tensors in the flat weight buffer.
+constexpr int kW_in = 0;
+constexpr int kB_in = kW_in + D * 4;
+constexpr int kLayer0 = kB_in + D;
+constexpr int kLayerSize = QKV * D + QKV + D * D + D + 2 * D + FF * D + FF + D * FF + D + 2 * D;
+constexpr int kW_qkv = 0, kB_qkv = kW_qkv + QKV * D, kW_o = kB_qkv + QKV, kB_o = kW_o + D * D;
+constexpr int kLn1g = kB_o + D, kLn1b = kLn1g + D, kW_1 = kLn1b + D, kB_1 = kW_1 + FF * D;
+constexpr int kW_2 = kB_1 + FF, kB_2 = kW_2 + D * FF, kLn2g = kB_2 + D, kLn2b = kLn2g + D;
+constexpr int kW_out = kLayer0 + kHeadLayers * kLayerSize;
+constexpr int kB_out = kW_out + D;
+static_assert(kLayerSize == 33472 && kB_out + 1 == kHeadWeights, "parameter layout");
+static_assert(kLn2b + D == kLayerSize, "layer layout");
+
+// Padded LDS row strides (floats): rows of a tile start on different banks.
+constexpr int kSA = D + 4;   // 64-wide activations and weights
+constexpr int kSF = FF + 4;  // 128-wide
+
+// Largest i with offsets[i] <= r (offsets non-decreasing, offsets[0] <= r).
+__device__ int64_t request_of(const int32_t* offsets, int32_t n_req, int64_t r) {
+  int64_t lo = 0, hi = n_req - 1;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) / 2;
+    if (offsets[mid] <= r) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+// C (64 x 16*NB) += A (64 x K, LDS, stride sa) x B^T, B = W (16*NB rows x K,
+// LDS, stride sw): wave w computes row block w; acc[j] is column block j in
+// the MFMA output layout (lane l, register r: row 4*(l/16) + r, column l%16
+// of the 16 x 16 block).
+template <int NB, int K>
+__device__ __forceinline__ void tile_gemm(const float* A, int sa, const float* W, int sw, f4 (&acc)[NB]) {
+  const int lane = threadIdx.x % kWave;
+  const int w = threadIdx.x / kWave;
+  const int ar = 16 * w + lane % 16;
+  const int kq = lane / 16;
+#pragma unroll 4
+  for (int k0 = 0; k0 < K; k0 += 4) {
+    const float a = A[ar * sa + k0 + kq];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const float b = W[(16 * j + lane % 16) * sw + k0 + kq];
+      acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[j], 0, 0, 0);
+    }
+  }
+}
+
+// Copies rows x cols floats (row-major, global) into LDS with row stride s.
+__device__ __forceinline__ void stage(float* dst, int s, const float* src, int rows, int cols) {
+  for (int i = threadIdx.x; i < rows * cols; i += kTileThreads) dst[(i / cols) * s + i % cols] = src[i];
+}
+
+// LayerNorm of the 64 values of each row held by the 16 lanes l / 16 = q of a
+// wave (4 column blocks x 4 rows per lane, MFMA layout): x[j][r] is row
+// 4q + r, column 16 j + l % 16. Biased variance, eps 1e-5.
+__device__ __forceinline__ void layer_norm_rows(f4 (&x)[4], const float* g, const float* b) {
+  const int c = threadIdx.x % 16;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float s = x[0][r] + x[1][r] + x[2][r] + x[3][r];
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) s += __shfl_xor(s, o, 16);
+    const float mu = s * (1.0f / D);
+    float v = 0.0f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float d = x[j][r] - mu;
+      v = fmaf(d, d, v);
+    }
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) v += __shfl_xor(v, o, 16);
+    const float inv = 1.0f / sqrtf(v * (1.0f / D) + kLnEps);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) x[j][r] = fmaf((x[j][r] - mu) * inv, g[16 * j + c], b[16 * j + c]);
+  }
+}
+
+}  // namespace
+
+// QKV projection of a 64-row tile; FIRST: the rows are made from X first
+// (projection + positional encoding) and written to H.
+template <bool FIRST>
+__global__ __launch_bounds__(kTileThreads) void head_qkv_kernel(HeadArgs a, int layer, const float* Hin,
+                                                               float* Hout) {
+  __shared__ float sA[kTile * kSA];
+  __shared__ float sW[QKV * kSA];
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kTile;
+  const float* Wl = a.weights + kLayer0 + layer * kLayerSize;
+  if (FIRST) {
+    // row position t - 1 within its request, one thread per row
+    __shared__ int32_t sPos[kTile];
+    if (threadIdx.x < kTile) {
+      const int64_t r = r0 + threadIdx.x;
+      int32_t pos = 0;
+      if (r < a.n_rows) pos = static_cast<int32_t>(r - a.offsets[request_of(a.offsets, a.n_req, r)]);
+      sPos[threadIdx.x] = pos;
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < kTile * D; i += kTileThreads) {
+      const int rr = i / D, j = i % D;
+      const int64_t r = r0 + rr;
+      float h = 0.0f;
+      if (r < a.n_rows) {
+        const float* x = a.X + r * 4;
+        const float* w = a.weights + kW_in + j * 4;
+        h = a.weights[kB_in + j];
+        h = fmaf(w[0], x[0], h);
+        h = fmaf(w[1], x[1], h);
+        h = fmaf(w[2], x[2], h);
+        h = fmaf(w[3], x[3], h);
+        // sinusoid of position t - 1 (angles in float64: positions reach 10^3)
+        const int i2 = j & ~1;
+        const double angle = static_cast<double>(sPos[rr]) * exp2(-static_cast<double>(i2) / D * 13.287712379549449);
+        h += static_cast<float>((j & 1) ? cos(angle) : sin(angle));
+        Hout[r * D + j] = h;
+      }
+      sA[rr * kSA + j] = h;
+    }
+  } else {
+    for (int i = threadIdx.x; i < kTile * D; i += kTileThreads) {
+      const int64_t r = r0 + i / D;
+      sA[(i / D) * kSA + i % D] = r < a.n_rows ? Hin[r * D + i % D] : 0.0f;
+    }
+  }
+  stage(sW, kSA, Wl + kW_qkv, QKV, D);
+  __syncthreads();
+  f4 acc[QKV / 16];
+#pragma unroll
+  for (int j = 0; j < QKV / 16; ++j) acc[j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+  tile_gemm<QKV / 16, D>(sA, kSA, sW, kSA, acc);
+  const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+#pragma unroll
+  for (int j = 0; j < QKV / 16; ++j) {
+    const int col = 16 * j + lane % 16;
+    const float bias = Wl[kB_qkv + col];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t row = r0 + 16 * w + 4 * (lane / 16) + r;
+      if (row < a.n_rows) a.qkv[row * QKV + col] = acc[j][r] + bias;
+    }
+  }
+}
+
+// Scaled dot-product attention of 64 queries (one per lane) of one request
+// and one head over all of the request's keys. The 4 waves of the workgroup
+// take turns over the key tiles of 64 (staged in each wave's own LDS, read
+// as 16-byte vectors), each keeping an online softmax in base 2 (queries
+// pre-scaled by log2(e) / sqrt(16)); the 4 partial states are then merged
+// through LDS in a fixed order.
+constexpr int kAttnWaves = 4;
+
+__global__ __launch_bounds__(kAttnWaves * kWave) void head_attn_kernel(HeadArgs a) {
+  __shared__ f4 sK[kAttnWaves][kWave * DH / 4];
+  __shared__ f4 sV[kAttnWaves][kWave * DH / 4];
+  __shared__ float sM[kAttnWaves][kWave], sL[kAttnWaves][kWave];
+  __shared__ f4 sAcc[kAttnWaves][DH / 4][kWave];
+  const int64_t req = blockIdx.x;
+  const int hd = blockIdx.y;
+  const int64_t lo = a.offsets[req], hi = a.offsets[req + 1];
+  const int64_t T = hi - lo;
+  if (T > a.max_len) return;  // scored NaN by the pool kernel
+  const int64_t q0 = lo + static_cast<int64_t>(blockIdx.z) * kWave;
+  if (q0 >= hi) return;
+  const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+  const int64_t q = q0 + lane;
+  const bool valid = q < hi;
+  constexpr float kScale = 1.4426950408889634f / 4.0f;  // log2(e) / sqrt(DH)
+  float qv[DH];
+#pragma unroll
+  for (int d = 0; d < DH; ++d) qv[d] = valid ? a.qkv[q * QKV + hd * DH + d] * kScale : 0.0f;
+  float m = -INFINITY, l = 0.0f, acc[DH];
+#pragma unroll
+  for (int d = 0; d < DH; ++d) acc[d] = 0.0f;
+  f4* K = sK[w];
+  f4* Vt = sV[w];
+  for (int64_t k0 = lo + static_cast<int64_t>(w) * kWave; k0 < hi; k0 += kAttnWaves * kWave) {
+    const int nk = static_cast<int>(hi - k0 < kWave ? hi - k0 : kWave);
+    // wave-private tile: the wave's own LDS ops complete in order
+    if (lane < nk) {
+      const f4* src = reinterpret_cast<const f4*>(a.qkv + (k0 + lane) * QKV);
+#pragma unroll
+      for (int d4 = 0; d4 < DH / 4; ++d4) {
+        K[lane * (DH / 4) + d4] = src[(D + hd * DH) / 4 + d4];
+        Vt[lane * (DH / 4) + d4] = src[(2 * D + hd * DH) / 4 + d4];
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    for (int j0 = 0; j0 < nk; j0 += 8) {
+      const int nj = nk - j0 < 8 ? nk - j0 : 8;
+      float s[8];
+      float smax = -INFINITY;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        float t = -INFINITY;
+        if (u < nj) {
+          t = 0.0f;
+#pragma unroll
+          for (int d4 = 0; d4 < DH / 4; ++d4) {
+            const f4 k = K[(j0 + u) * (DH / 4) + d4];
+            t = fmaf(qv[4 * d4], k.x, t);
+            t = fmaf(qv[4 * d4 + 1], k.y, t);
+            t = fmaf(qv[4 * d4 + 2], k.z, t);
+            t = fmaf(qv[4 * d4 + 3], k.w, t);
+          }
+        }
+        s[u] = t;
+        smax = fmaxf(smax, t);
+      }
+      const float mn = fmaxf(m, smax);
+      const float corr = exp2f(m - mn);  // m = -inf at first: 0
+      l *= corr;
+#pragma unroll
+      for (int d = 0; d < DH; ++d) acc[d] *= corr;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (u < nj) {
+          const float p = exp2f(s[u] - mn);
+          l += p;
+#pragma unroll
+          for (int d4 = 0; d4 < DH / 4; ++d4) {
+            const f4 v = Vt[(j0 + u) * (DH / 4) + d4];
+            acc[4 * d4] = fmaf(p, v.x, acc[4 * d4]);
+            acc[4 * d4 + 1] = fmaf(p, v.y, acc[4 * d4 + 1]);
+            acc[4 * d4 + 2] = fmaf(p, v.z, acc[4 * d4 + 2]);
+            acc[4 * d4 + 3] = fmaf(p, v.w, acc[4 * d4 + 3]);
+          }
+        }
+      }
+      m = mn;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();  // the tile is read before the next one overwrites it
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  sM[w][lane] = m;
+  sL[w][lane] = l;
+#pragma unroll
+  for (int d4 = 0; d4 < DH / 4; ++d4) sAcc[w][d4][lane] = f4{acc[4 * d4], acc[4 * d4 + 1], acc[4 * d4 + 2], acc[4 * d4 + 3]};
+  __syncthreads();
+  if (w == 0 && valid) {
+    float M = sM[0][lane];
+#pragma unroll
+    for (int k = 1; k < kAttnWaves; ++k) M = fmaxf(M, sM[k][lane]);
+    float L = 0.0f;
+    f4 o[DH / 4];
+#pragma unroll
+    for (int d4 = 0; d4 < DH / 4; ++d4) o[d4] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int k = 0; k < kAttnWaves; ++k) {
+      const float c = sM[k][lane] == -INFINITY ? 0.0f : exp2f(sM[k][lane] - M);  // a wave with no keys adds nothing
+      L = fmaf(sL[k][lane], c, L);
+#pragma unroll
+      for (int d4 = 0; d4 < DH / 4; ++d4) o[d4] += sAcc[k][d4][lane] * c;
+    }
+    const float inv = 1.0f / L;
+    f4* dst = reinterpret_cast<f4*>(a.att + q * D + hd * DH);
+#pragma unroll
+    for (int d4 = 0; d4 < DH / 4; ++d4) dst[d4] = o[d4] * inv;
+  }
+}
+
+// Output projection, residual and LayerNorm, feed-forward, residual and
+// LayerNorm of a 64-row tile.
+__global__ __launch_bounds__(kTileThreads) void head_ffn_kernel(HeadArgs a, int layer, const float* Hin,
+                                                               float* Hout) {
+  __shared__ float sA[kTile * kSA];   // attention output, then h1
+  __shared__ float sF[kTile * kSF];   // feed-forward hidden layer
+  __shared__ float sW[FF * kSA];      // W_o, W_1, W_2 in turn (W_2 as 64 x 128)
+  const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kTile;
+  const float* Wl = a.weights + kLayer0 + layer * kLayerSize;
+  const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+  for (int i = threadIdx.x; i < kTile * D; i += kTileThreads) {
+    const int64_t r = r0 + i / D;
+    sA[(i / D) * kSA + i % D] = r < a.n_rows ? a.att[r * D + i % D] : 0.0f;
+  }
+  stage(sW, kSA, Wl + kW_o, D, D);
+  __syncthreads();
+  // y = att W_o^T + b_o + h; h1 = LN1(y)
+  f4 y[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) y[j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+  tile_gemm<4, D>(sA, kSA, sW, kSA, y);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int col = 16 * j + lane % 16;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t row = r0 + 16 * w + 4 * (lane / 16) + r;
+      y[j][r] += Wl[kB_o + col] + (row < a.n_rows ? Hin[row * D + col] : 0.0f);
+    }
+  }
+  layer_norm_rows(y, Wl + kLn1g, Wl + kLn1b);
+  __syncthreads();  // everyone is done reading sA and sW
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sA[(16 * w + 4 * (lane / 16) + r) * kSA + 16 * j + lane % 16] = y[j][r];
+  stage(sW, kSA, Wl + kW_1, FF, D);
+  __syncthreads();
+  // f = relu(h1 W_1^T + b_1)
+  {
+    f4 f[FF / 16];
+#pragma unroll
+    for (int j = 0; j < FF / 16; ++j) f[j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    tile_gemm<FF / 16, D>(sA, kSA, sW, kSA, f);
+#pragma unroll
+    for (int j = 0; j < FF / 16; ++j) {
+      const int col = 16 * j + lane % 16;
+      const float bias = Wl[kB_1 + col];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sF[(16 * w + 4 * (lane / 16) + r) * kSF + col] = fmaxf(f[j][r] + bias, 0.0f);
+    }
+  }
+  __syncthreads();  // sF complete, sW free
+  stage(sW, kSF, Wl + kW_2, D, FF);
+  __syncthreads();
+  // z = f W_2^T + b_2 + h1; h2 = LN2(z)
+  f4 z[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) z[j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+  tile_gemm<4, FF>(sF, kSF, sW, kSF, z);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int col = 16 * j + lane % 16;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) z[j][r] += Wl[kB_2 + col] + y[j][r];
+  }
+  layer_norm_rows(z, Wl + kLn2g, Wl + kLn2b);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int col = 16 * j + lane % 16;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t row = r0 + 16 * w + 4 * (lane / 16) + r;
+      if (row < a.n_rows) Hout[row * D + col] = z[j][r];
+    }
+  }
+}
+
+// Mean pool of a request's rows, linear map to one logit, sigmoid. An empty
+// request, or one longer than max_len, scores NaN.
+constexpr int kPoolThreads = 1024;
+
+__global__ __launch_bounds__(kPoolThreads) void head_pool_kernel(HeadArgs a, const float* H) {
+  __shared__ float part[kPoolThreads / D][D];
+  const int64_t req = blockIdx.x;
+  const int64_t lo = a.offsets[req], hi = a.offsets[req + 1];
+  const int64_t T = hi - lo;
+  const int c = threadIdx.x % D, p = threadIdx.x / D;
+  float s = 0.0f;
+  for (int64_t r = lo + p; r < hi; r += kPoolThreads / D) s += H[r * D + c];
+  part[p][c] = s;
+  __syncthreads();
+  if (threadIdx.x < kWave) {
+    float t = 0.0f;
+    for (int k = 0; k < kPoolThreads / D; ++k) t += part[k][threadIdx.x];
+    const float mean = t / static_cast<float>(T > 0 ? T : 1);
+    float z = mean * a.weights[kW_out + threadIdx.x];
+    z = wave_sum(z) + a.weights[kB_out];
+    if (threadIdx.x == 0)
+      a.scores[req] = (T <= 0 || T > a.max_len) ? __uint_as_float(0x7fc00000u) : 1.0f / (1.0f + expf(-z));
+  }
+}
+
+size_t head_workspace_bytes(int64_t n_rows) {
+  return static_cast<size_t>(n_rows) * (2 * D + QKV + D) * sizeof(float);
+}
+
+hipError_t launch_head(const HeadArgs& args, hipStream_t stream) {
+  if (args.n_req == 0) return hipSuccess;
+  HeadArgs a = args;
+  float* H0 = a.ws;
+  float* H1 = H0 + a.n_rows * D;
+  a.qkv = H1 + a.n_rows * D;
+  a.att = a.qkv + a.n_rows * QKV;
+  const unsigned tiles = static_cast<unsigned>((a.n_rows + kTile - 1) / kTile);
+  const dim3 attn_grid(static_cast<unsigned>(a.n_req), NH, static_cast<unsigned>((a.max_len + kWave - 1) / kWave));
+  if (a.n_rows > 0) {
+    float* Hin = H0;
+    float* Hout = H1;
+    for (int l = 0; l < kHeadLayers; ++l) {
+      if (l == 0)
+        head_qkv_kernel<true><<<tiles, kTileThreads, 0, stream>>>(a, 0, nullptr, Hin);
+      else
+        head_qkv_kernel<false><<<tiles, kTileThreads, 0, stream>>>(a, l, Hin, nullptr);
+      head_attn_kernel<<<attn_grid, kAttnWaves * kWave, 0, stream>>>(a);
+      head_ffn_kernel<<<tiles, kTileThreads, 0, stream>>>(a, l, Hin, Hout);
+      float* t = Hin;
+      Hin = Hout;
+      Hout = t;
+    }
+    head_pool_kernel<<<static_cast<unsigned>(a.n_req), kPoolThreads, 0, stream>>>(a, Hin);
+  } else {
+    head_pool_kernel<<<static_cast<unsigned>(a.n_req), kPoolThreads, 0, stream>>>(a, H0);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace pr

@@ -146,3 +146,17 @@ def test_feature_sequence_zero_rows_is_valid():
     from paper_2608_28726_amd import _abi
     assert lib.pr_feature_sequence(None, 1, 0, 100, 100, None, None, None, None, 0, 20, None, None, None) == \
         _abi.PR_OK
+
+
+def test_verifier_head_rejects_bad_arguments():
+    lib = ensure_built()
+    from paper_2608_28726_amd import _abi
+    p = C.c_void_p(256)
+    ws = int(lib.pr_verifier_head_workspace(10))
+    assert ws == 10 * (2 * 64 + 192 + 64) * 4
+    assert lib.pr_verifier_head(p, 10, p, 2, 0, p, p, p, ws, None) == _abi.PR_ERR_INVALID_ARG      # max_len < 1
+    assert lib.pr_verifier_head(p, -1, p, 2, 8, p, p, p, ws, None) == _abi.PR_ERR_INVALID_ARG      # n_rows < 0
+    assert lib.pr_verifier_head(p, 10, None, 2, 8, p, p, p, ws, None) == _abi.PR_ERR_INVALID_ARG   # offsets
+    assert lib.pr_verifier_head(p, 10, p, 2, 8, None, p, p, ws, None) == _abi.PR_ERR_INVALID_ARG   # weights
+    assert lib.pr_verifier_head(p, 10, p, 2, 8, p, p, p, ws - 1, None) == _abi.PR_ERR_INVALID_ARG  # workspace
+    assert lib.pr_verifier_head(None, 0, None, 0, 8, None, None, None, 0, None) == _abi.PR_OK       # nothing to do
