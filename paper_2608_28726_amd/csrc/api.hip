@@ -157,7 +157,7 @@ pr_status pr_verifier_head(const float* X, int64_t n_rows, const int32_t* offset
   if (n_rows < 0 || n_req < 0 || max_len < 1) return PR_ERR_INVALID_ARG;
   if (n_rows > (int64_t{1} << 30)) return PR_ERR_UNSUPPORTED;
   if (n_req == 0) return PR_OK;
-  if (!offsets || !weights || !scores) return PR_ERR_INVALID_ARG;
+  if (!offsets || !weights || !scores || !aligned(weights, 16)) return PR_ERR_INVALID_ARG;
   if (n_rows > 0 && (!X || !aligned(X, 4))) return PR_ERR_INVALID_ARG;
   const size_t need = pr_verifier_head_workspace(n_rows);
   if (need > 0 && (!workspace || workspace_bytes < need || !aligned(workspace, 16))) return PR_ERR_INVALID_ARG;

@@ -81,9 +81,41 @@ __device__ __forceinline__ void tile_gemm(const float* A, int sa, const float* W
   }
 }
 
-// Copies rows x cols floats (row-major, global) into LDS with row stride s.
-__device__ __forceinline__ void stage(float* dst, int s, const float* src, int rows, int cols) {
-  for (int i = threadIdx.x; i < rows * cols; i += kTileThreads) dst[(i / cols) * s + i % cols] = src[i];
+// Copies ROWS x COLS floats (row-major, global) into LDS with row stride S,
+// as 16-byte vectors: every load of a thread is issued before its first
+// store, so the copy costs one memory round trip.
+template <int ROWS, int COLS, int S>
+__device__ __forceinline__ void stage(float* dst, const float* src) {
+  constexpr int kVecs = ROWS * COLS / 4;
+  static_assert(kVecs % kTileThreads == 0 && COLS % 4 == 0 && S % 4 == 0, "whole vectors per thread");
+  constexpr int kPer = kVecs / kTileThreads;
+  const f4* s4 = reinterpret_cast<const f4*>(src);
+  f4 v[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) v[k] = s4[threadIdx.x + k * kTileThreads];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int i = threadIdx.x + k * kTileThreads;
+    *reinterpret_cast<f4*>(dst + (i / (COLS / 4)) * S + (i % (COLS / 4)) * 4) = v[k];
+  }
+}
+
+// The same for rows r0 .. r0+63 of a [n_rows][64] activation array (rows
+// past the end read as zero).
+__device__ __forceinline__ void stage_rows(float* dst, const float* src, int64_t r0, int64_t n_rows) {
+  constexpr int kPer = kTile * D / 4 / kTileThreads;
+  f4 v[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int i = threadIdx.x + k * kTileThreads;
+    const int64_t r = r0 + i / (D / 4);
+    v[k] = r < n_rows ? reinterpret_cast<const f4*>(src + r * D)[i % (D / 4)] : f4{0.0f, 0.0f, 0.0f, 0.0f};
+  }
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int i = threadIdx.x + k * kTileThreads;
+    *reinterpret_cast<f4*>(dst + (i / (D / 4)) * kSA + (i % (D / 4)) * 4) = v[k];
+  }
 }
 
 // LayerNorm of the 64 values of each row held by the 16 lanes l / 16 = q of a
@@ -153,12 +185,9 @@ __global__ __launch_bounds__(kTileThreads) void head_qkv_kernel(HeadArgs a, int 
       sA[rr * kSA + j] = h;
     }
   } else {
-    for (int i = threadIdx.x; i < kTile * D; i += kTileThreads) {
-      const int64_t r = r0 + i / D;
-      sA[(i / D) * kSA + i % D] = r < a.n_rows ? Hin[r * D + i % D] : 0.0f;
-    }
+    stage_rows(sA, Hin, r0, a.n_rows);
   }
-  stage(sW, kSA, Wl + kW_qkv, QKV, D);
+  stage<QKV, D, kSA>(sW, Wl + kW_qkv);
   __syncthreads();
   f4 acc[QKV / 16];
 #pragma unroll
@@ -202,8 +231,17 @@ __global__ __launch_bounds__(kAttnWaves * kWave) void head_attn_kernel(HeadArgs 
   const bool valid = q < hi;
   constexpr float kScale = 1.4426950408889634f / 4.0f;  // log2(e) / sqrt(DH)
   float qv[DH];
+  {
+    const f4* qp = reinterpret_cast<const f4*>(a.qkv + (valid ? q : lo) * QKV + hd * DH);
 #pragma unroll
-  for (int d = 0; d < DH; ++d) qv[d] = valid ? a.qkv[q * QKV + hd * DH + d] * kScale : 0.0f;
+    for (int d4 = 0; d4 < DH / 4; ++d4) {
+      const f4 t = qp[d4] * kScale;
+      qv[4 * d4] = t.x;
+      qv[4 * d4 + 1] = t.y;
+      qv[4 * d4 + 2] = t.z;
+      qv[4 * d4 + 3] = t.w;
+    }
+  }
   float m = -INFINITY, l = 0.0f, acc[DH];
 #pragma unroll
   for (int d = 0; d < DH; ++d) acc[d] = 0.0f;
@@ -307,11 +345,8 @@ __global__ __launch_bounds__(kTileThreads) void head_ffn_kernel(HeadArgs a, int 
   const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kTile;
   const float* Wl = a.weights + kLayer0 + layer * kLayerSize;
   const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
-  for (int i = threadIdx.x; i < kTile * D; i += kTileThreads) {
-    const int64_t r = r0 + i / D;
-    sA[(i / D) * kSA + i % D] = r < a.n_rows ? a.att[r * D + i % D] : 0.0f;
-  }
-  stage(sW, kSA, Wl + kW_o, D, D);
+  stage_rows(sA, a.att, r0, a.n_rows);
+  stage<D, D, kSA>(sW, Wl + kW_o);
   __syncthreads();
   // y = att W_o^T + b_o + h; h1 = LN1(y)
   f4 y[4];
@@ -333,7 +368,7 @@ __global__ __launch_bounds__(kTileThreads) void head_ffn_kernel(HeadArgs a, int 
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int r = 0; r < 4; ++r) sA[(16 * w + 4 * (lane / 16) + r) * kSA + 16 * j + lane % 16] = y[j][r];
-  stage(sW, kSA, Wl + kW_1, FF, D);
+  stage<FF, D, kSA>(sW, Wl + kW_1);
   __syncthreads();
   // f = relu(h1 W_1^T + b_1)
   {
@@ -350,7 +385,7 @@ __global__ __launch_bounds__(kTileThreads) void head_ffn_kernel(HeadArgs a, int 
     }
   }
   __syncthreads();  // sF complete, sW free
-  stage(sW, kSF, Wl + kW_2, D, FF);
+  stage<D, FF, kSF>(sW, Wl + kW_2);
   __syncthreads();
   // z = f W_2^T + b_2 + h1; h2 = LN2(z)
   f4 z[4];

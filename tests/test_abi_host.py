@@ -158,5 +158,6 @@ def test_verifier_head_rejects_bad_arguments():
     assert lib.pr_verifier_head(p, -1, p, 2, 8, p, p, p, ws, None) == _abi.PR_ERR_INVALID_ARG      # n_rows < 0
     assert lib.pr_verifier_head(p, 10, None, 2, 8, p, p, p, ws, None) == _abi.PR_ERR_INVALID_ARG   # offsets
     assert lib.pr_verifier_head(p, 10, p, 2, 8, None, p, p, ws, None) == _abi.PR_ERR_INVALID_ARG   # weights
+    assert lib.pr_verifier_head(p, 10, p, 2, 8, C.c_void_p(260), p, p, ws, None) == _abi.PR_ERR_INVALID_ARG
     assert lib.pr_verifier_head(p, 10, p, 2, 8, p, p, p, ws - 1, None) == _abi.PR_ERR_INVALID_ARG  # workspace
     assert lib.pr_verifier_head(None, 0, None, 0, 8, None, None, None, 0, None) == _abi.PR_OK       # nothing to do
