@@ -28,8 +28,13 @@ R22  P-square, as published, with two readings: the desired marker positions
      accumulated increments (the same values without accumulated rounding);
      and with at most 5 observations (the markers are then the sorted
      observations themselves) the estimate is their exact nearest-rank
-     p-quantile, as for the exact summary (R8), not the middle marker. A NaN observation is not fed to the markers (the
-     feature's summaries are NaN anyway, R9).
+     p-quantile, as for the exact summary (R8), not the middle marker. A
+     NaN observation is not fed to the markers (the feature's summaries are
+     NaN anyway, R9). Nor is an infinite one (a margin of +inf from a row
+     with one finite logit, a log-prob of -inf): the interpolation is not
+     defined on infinite heights (inf - inf), so the estimate becomes NaN
+     for the rest of the request and a score that uses it escalates; the
+     mean and minimum still include the value.
 """
 
 from __future__ import annotations
@@ -63,10 +68,16 @@ class P2Quantile:
         self.q = []          # marker heights (the first observations until there are 5)
         self.n = [1, 2, 3, 4, 5]  # marker positions (1-based)
         self.count = 0
+        self.poisoned = False  # an infinite observation was seen
 
     def add(self, x: float) -> None:
         x = float(x)
         if math.isnan(x):
+            return
+        if math.isinf(x):
+            self.poisoned = True
+            return
+        if self.poisoned:
             return
         self.count += 1
         if self.count <= 5:
@@ -75,12 +86,14 @@ class P2Quantile:
                 self.q.sort()
             return
         q, n = self.q, self.n
-        # the cell holding x; the extreme markers follow the extremes
+        # the cell k with q[k] <= x < q[k+1]; the extreme markers follow the
+        # extremes (the maximum is replaced only by a larger value)
         if x < q[0]:
             q[0] = x
             k = 0
         elif x >= q[4]:
-            q[4] = max(q[4], x)
+            if x > q[4]:
+                q[4] = x
             k = 3
         else:
             k = 0
@@ -105,7 +118,7 @@ class P2Quantile:
                 n[i] += s
 
     def estimate(self) -> float:
-        if self.count == 0:
+        if self.count == 0 or self.poisoned:
             return math.nan
         if self.count <= 5:
             v = sorted(self.q)

@@ -140,7 +140,24 @@ def pin_p2_ties(mod):
     return fails
 
 
-ALL = [pin_calibrate, pin_p2_small, pin_p2_linear, pin_p2_affine, pin_p2_convergence,
+def pin_p2_nonfinite(mod):
+    """NaN is skipped; an infinite observation makes the estimate NaN."""
+    fails = []
+    v = list(np.random.default_rng(7).normal(0, 1, 50))
+    base = mod.p2_quantile(v, 0.3)
+    if mod.p2_quantile(v[:20] + [math.nan] + v[20:], 0.3) != base:
+        fails.append("a NaN observation changed the estimate")
+    for bad in (math.inf, -math.inf):
+        for at in (2, 30):
+            e = mod.p2_quantile(v[:at] + [bad] + v[at:], 0.3)
+            if not math.isnan(e):
+                fails.append(f"{bad} at {at}: estimate {e}")
+    if not math.isnan(mod.p2_quantile([], 0.5)) or not math.isnan(mod.p2_quantile([math.nan], 0.5)):
+        fails.append("empty stream")
+    return fails
+
+
+ALL = [pin_calibrate, pin_p2_nonfinite, pin_p2_small, pin_p2_linear, pin_p2_affine, pin_p2_convergence,
        pin_p2_published_example, pin_p2_ties]
 
 
@@ -157,6 +174,7 @@ MUTANTS = {
     "marker targets": ("self.f = (0.0, self.p / 2.0, self.p, (1.0 + self.p) / 2.0, 1.0)",
                        "self.f = (0.0, self.p, self.p, (1.0 + self.p) / 2.0, 1.0)"),
     "cell boundary": ("while not (q[k] <= x < q[k + 1]):", "while not (q[k] < x <= q[k + 1]):"),
+    "infinity fed": ("        if math.isinf(x):\n            self.poisoned = True\n            return\n", ""),
     "parabola sign": ("(n[i] - n[i - 1] + s) * (q[i + 1] - q[i])", "(n[i] - n[i - 1] - s) * (q[i + 1] - q[i])"),
     "linear neighbour": ("qp = q[i] + s * (q[i + s] - q[i]) / (n[i + s] - n[i])",
                          "qp = q[i] + s * (q[i - s] - q[i]) / (n[i - s] - n[i])"),
@@ -176,4 +194,11 @@ def _mutant(old, new):
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_mutant_is_caught(name):
     mod = _mutant(*MUTANTS[name])
-    assert any(pin(mod) for pin in ALL), f"mutant '{name}' passed every pin"
+
+    def fails(pin):
+        try:
+            return bool(pin(mod))
+        except (IndexError, ValueError, ZeroDivisionError):
+            return True
+
+    assert any(fails(pin) for pin in ALL), f"mutant '{name}' passed every pin"
