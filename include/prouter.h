@@ -241,6 +241,22 @@ pr_status pr_route(const float* scores, int32_t n_req, float threshold, uint8_t*
                    void* stream);
 
 /*
+ * Threshold calibration for a ship fraction (Sec. 3.1: tau is fixed in
+ * advance by calibration on a validation pool; Sec. 4.1: the coverage rule,
+ * a fraction q of the pool ships). scores: device float32 [n], the pool's
+ * shipping confidences; NaN scores are not part of the pool (they always
+ * escalate). tau[0] (device float32) = the k-th largest of the n_valid
+ * non-NaN scores, k = max(1, ceil(ship_fraction * n_valid)) with the product
+ * rounded once in double; n_ship[0] (device int32, may be NULL) =
+ * #{scores >= tau}, at least k (more when scores tie at tau). -0 counts as
+ * +0. ship_fraction == 0 or no valid score: tau = +inf, n_ship = 0.
+ * ship_fraction must lie in [0, 1] (NaN rejected); n >= 0; scores may be
+ * NULL only when n == 0. Exact: tau is one of the scores.
+ */
+pr_status pr_calibrate_threshold(const float* scores, int32_t n, double ship_fraction, float* tau, int32_t* n_ship,
+                                 void* stream);
+
+/*
  * Synchronous debug check of an offsets array (device pointer): returns
  * PR_OK iff offsets[0] == 0, offsets are non-decreasing and
  * offsets[n_req] == n_rows. Synchronises `stream`.
@@ -259,6 +275,12 @@ typedef struct pr_stream pr_stream;
  * Allocates the device state for max_slots concurrent requests of at most
  * max_len tokens each, on the current device (the only allocating call of
  * the streaming API). params may be NULL (defaults). *state is a host handle.
+ * max_len == 0 selects bounded memory: no per-token history is kept and the
+ * tail quantile is the P-square estimate of the params' q (Jain and
+ * Chlamtac, CACM 1985), 224 bytes per slot, any number of tokens per
+ * request. Its estimate is exact up to 5 tokens; an infinite value of a
+ * column (a margin of +inf, a log-prob of -inf) makes that column's
+ * quantile NaN for the request (the mean and minimum keep it).
  */
 pr_status pr_stream_create(int32_t max_slots, int32_t max_len, const pr_agg_params* params, pr_stream** state);
 
@@ -269,7 +291,8 @@ pr_status pr_stream_create(int32_t max_slots, int32_t max_len, const pr_agg_para
  * and the token's A is appended to the slot's history (needed for the exact
  * quantile). A slot may appear at most once per step (duplicates race).
  * Tokens past max_len are counted in sums and minima but not kept, and the
- * slot's quantile becomes NaN. out may be NULL (features not returned).
+ * slot's quantile becomes NaN. In bounded-memory mode (max_len == 0) the
+ * token instead updates the slot's P-square markers. out may be NULL (features not returned).
  * top_p must be NULL (PR_ERR_UNSUPPORTED otherwise).
  */
 pr_status pr_stream_step(pr_stream* state, const void* logits, pr_dtype dtype, int32_t n_active,

@@ -25,7 +25,8 @@ from . import _abi
 from ._abi import (FLAG_BAD_ID, FLAG_BAD_TP, FLAG_NONFINITE, FLAG_OUTSIDE_NUCLEUS,  # noqa: F401
                    ProuterError)
 
-__all__ = ["token_features", "feature_sequence", "verifier_head", "request_aggregate", "route", "validate_offsets", "StreamState",
+__all__ = ["token_features", "feature_sequence", "verifier_head", "request_aggregate", "route", "calibrate_threshold",
+           "validate_offsets", "StreamState",
            "token_features_workspace", "ProuterError", "FEATURE_FLOATS", "FEATURE_INTS", "PAPER_TOP_K"]
 
 PAPER_TOP_K = 20  # K of the paper's top-K entropy (Sec. 3.1)
@@ -223,6 +224,19 @@ def route(scores: torch.Tensor, threshold: float):
     return ship, n_ship
 
 
+def calibrate_threshold(scores: torch.Tensor, ship_fraction: float):
+    """Threshold tau for a ship fraction on a validation pool of scores
+    (``pr_calibrate_threshold``). Returns (tau float32 [1], n_ship int32 [1])."""
+    if scores.dtype != torch.float32 or not scores.is_cuda or not scores.is_contiguous() or scores.dim() != 1:
+        raise ValueError("scores must be a 1-D contiguous float32 CUDA tensor")
+    tau = torch.empty(1, dtype=torch.float32, device=scores.device)
+    n_ship = torch.empty(1, dtype=torch.int32, device=scores.device)
+    st = _abi.lib().pr_calibrate_threshold(_ptr(scores), scores.shape[0], float(ship_fraction), _ptr(tau),
+                                          _ptr(n_ship), _stream_handle())
+    _abi.check("pr_calibrate_threshold", st)
+    return tau, n_ship
+
+
 def validate_offsets(offsets: torch.Tensor, n_rows: int) -> bool:
     """Synchronous check of an offsets array (``pr_validate_offsets``)."""
     st = _abi.lib().pr_validate_offsets(_ptr(offsets), offsets.shape[0] - 1, n_rows, _stream_handle())
@@ -233,7 +247,10 @@ def validate_offsets(offsets: torch.Tensor, n_rows: int) -> bool:
 
 
 class StreamState:
-    """Device-resident per-request state for streaming decode (``pr_stream_*``)."""
+    """Device-resident per-request state for streaming decode (``pr_stream_*``).
+
+    ``max_len`` tokens of history per slot give the exact tail quantile;
+    ``max_len=0`` keeps P-square markers instead (bounded memory, any length)."""
 
     def __init__(self, max_slots: int, max_len: int, q: float = 0.1, weights=None, bias: float = 0.0,
                  link: str = "identity"):

@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OBJ_DIR = os.path.join(ROOT, "_build", "obj")
 LIB = os.path.join(PKG, "libprouter.so")
 
-SOURCES = ["row_features.hip", "topp.hip", "aggregate.hip", "head.hip", "api.hip"]
+SOURCES = ["row_features.hip", "topp.hip", "aggregate.hip", "head.hip", "calibrate.hip", "api.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

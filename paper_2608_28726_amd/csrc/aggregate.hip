@@ -11,6 +11,7 @@
 // batch (segments given by offsets) and the streaming state (each slot's
 // history).
 #include "aggregate.h"
+#include "p2.h"
 
 namespace pr {
 
@@ -274,12 +275,14 @@ __global__ void stream_clear_kernel(StreamDev s, const int32_t* slots, int32_t n
   for (int f = 0; f < 4; ++f) {
     s.sum[slot * 4 + f] = 0.0;
     s.minv[slot * 4 + f] = INFINITY;
+    if (s.p2q) p2::positions(s, slot, f)[12] = 0;
   }
 }
 
 // One workgroup per finishing slot: the running sums and minima come from the
 // slot state, the quantile is selected from the slot's history (wave f: column
-// f); then the slot is cleared.
+// f), or read from its P-square markers in bounded-memory mode; then the slot
+// is cleared.
 __global__ __launch_bounds__(kAggBlock) void stream_finish_kernel(StreamDev s, const int32_t* slots, int32_t n,
                                                                   AggParamsDev hp, float thr,
                                                                   pr_request_agg_t out, uint8_t* ship) {
@@ -302,7 +305,9 @@ __global__ __launch_bounds__(kAggBlock) void stream_finish_kernel(StreamDev s, c
     nanb = s.nanbits[slot];
   }
   float q = __uint_as_float(0x7fc00000u);
-  if (cnt > 0 && kept) {
+  if (s.p2q) {
+    if (cnt > 0) q = p2::estimate(s, slot, w);
+  } else if (cnt > 0 && kept) {
     const HistCol get{s.hist + (static_cast<int64_t>(slot) * 4 + w) * s.max_len};
     q = radix_select(get, 0, cnt, quant_rank(hp.q, cnt), sh.hist, sh.sel);
   }
@@ -323,6 +328,7 @@ __global__ __launch_bounds__(kAggBlock) void stream_finish_kernel(StreamDev s, c
       for (int f = 0; f < 4; ++f) {
         s.sum[slot * 4 + f] = 0.0;
         s.minv[slot * 4 + f] = INFINITY;
+        if (s.p2q) p2::positions(s, slot, f)[12] = 0;
       }
     }
   }

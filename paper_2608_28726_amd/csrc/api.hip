@@ -4,6 +4,7 @@
 #include <new>
 
 #include "aggregate.h"
+#include "calibrate.h"
 #include "head.h"
 #include "topp.h"
 
@@ -192,6 +193,13 @@ pr_status pr_route(const float* scores, int32_t n_req, float threshold, uint8_t*
   return hip_status(launch_route(scores, n_req, threshold, ship, n_ship, as_stream(stream)));
 }
 
+pr_status pr_calibrate_threshold(const float* scores, int32_t n, double ship_fraction, float* tau, int32_t* n_ship,
+                                 void* stream) {
+  if (n < 0 || !tau || (n > 0 && !scores)) return PR_ERR_INVALID_ARG;
+  if (!(ship_fraction >= 0.0 && ship_fraction <= 1.0)) return PR_ERR_INVALID_ARG;
+  return hip_status(launch_calibrate(scores, n, ship_fraction, tau, n_ship, as_stream(stream)));
+}
+
 pr_status pr_validate_offsets(const int32_t* offsets, int32_t n_req, int64_t n_rows, void* stream) {
   if (!offsets || n_req < 0) return PR_ERR_INVALID_ARG;
   int32_t* host = new (std::nothrow) int32_t[static_cast<size_t>(n_req) + 1];
@@ -210,7 +218,7 @@ pr_status pr_validate_offsets(const int32_t* offsets, int32_t n_req, int64_t n_r
 }
 
 pr_status pr_stream_create(int32_t max_slots, int32_t max_len, const pr_agg_params* params, pr_stream** state) {
-  if (!state || max_slots <= 0 || max_len <= 0) return PR_ERR_INVALID_ARG;
+  if (!state || max_slots <= 0 || max_len < 0) return PR_ERR_INVALID_ARG;
   *state = nullptr;
   const pr_agg_params p = params ? *params : default_params();
   if (!params_ok(p)) return PR_ERR_INVALID_ARG;
@@ -223,7 +231,10 @@ pr_status pr_stream_create(int32_t max_slots, int32_t max_len, const pr_agg_para
   const size_t b_min = up(S * 4 * sizeof(float));
   const size_t b_cnt = up(S * sizeof(int32_t));
   const size_t b_nan = up(S * sizeof(uint32_t));
-  const size_t total = b_ws + b_sum + b_hist + b_min + b_cnt + b_nan;
+  const bool bounded = max_len == 0;  // P-square markers instead of the history
+  const size_t b_p2q = bounded ? up(S * 20 * sizeof(double)) : 0;
+  const size_t b_p2n = bounded ? up(S * 16 * sizeof(int32_t)) : 0;
+  const size_t total = b_ws + b_sum + b_hist + b_min + b_cnt + b_nan + b_p2q + b_p2n;
   pr_stream* s = new (std::nothrow) pr_stream();
   if (!s) return PR_ERR_NO_MEMORY;
   hipError_t e = hipGetDevice(&s->device);
@@ -244,6 +255,12 @@ pr_status pr_stream_create(int32_t max_slots, int32_t max_len, const pr_agg_para
   s->dev.count = reinterpret_cast<int32_t*>(b);
   b += b_cnt;
   s->dev.nanbits = reinterpret_cast<uint32_t*>(b);
+  b += b_nan;
+  s->dev.p2q = bounded ? reinterpret_cast<double*>(b) : nullptr;
+  b += b_p2q;
+  s->dev.p2n = bounded ? reinterpret_cast<int32_t*>(b) : nullptr;
+  s->dev.p2p = p.q;
+  if (bounded) s->dev.hist = nullptr;
   s->dev.max_slots = max_slots;
   s->dev.max_len = max_len;
   s->params = p;

@@ -14,6 +14,11 @@ struct StreamDev {
   double* sum;        // [max_slots][4] running sums of A
   float* minv;        // [max_slots][4] running minima of A (+inf when empty)
   float* hist;        // [max_slots][4][max_len] every token's A, for the exact quantile
+  // Bounded-memory mode (max_len == 0, hist NULL): P-square markers instead
+  // of the history.
+  double* p2q;        // [max_slots][5][4] marker heights, NULL otherwise
+  int32_t* p2n;       // [max_slots][4][4] positions of markers 1..3, observations fed
+  double p2p;         // the quantile they track
 };
 
 // What the merge of a split row needs from the row besides the partial

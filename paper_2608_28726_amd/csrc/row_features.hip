@@ -15,6 +15,7 @@
 // decode state.
 #include <type_traits>
 
+#include "p2.h"
 #include "row_scan.h"
 #include "topk.h"
 
@@ -93,10 +94,13 @@ void row_features_kernel(RowArgs a) {
     }
     return;
   }
-  if (threadIdx.x == 0) {
+  if (threadIdx.x < kWave) {
     float conf[4];
-    finalize_row(a, r, p, cx, fix, conf);
-    stream_update(a.st, kEarlySlot ? ss : slot_load(a, r), conf);
+    if (threadIdx.x == 0) {
+      finalize_row(a, r, p, cx, fix, conf);
+      stream_update(a.st, kEarlySlot ? ss : slot_load(a, r), conf);
+    }
+    if (a.slot_ids && a.st.p2q) p2::feed_row(a, r, conf);
   }
 }
 
@@ -144,11 +148,12 @@ __global__ __launch_bounds__(kWave) void row_merge_kernel(RowArgs a) {
   p.t2 = q.t2;
   p.cnt = wave_sum_u(q.cnt);
   p.pad = 0;
+  float conf[4];
   if (lane == 0) {
-    float conf[4];
     finalize_row(a, r, p, cx, meta.fix, conf);
     stream_update(a.st, ss, conf);
   }
+  if (a.slot_ids && a.st.p2q) p2::feed_row(a, r, conf);
 }
 
 namespace {

@@ -99,6 +99,7 @@ def test_other_entry_points_reject_bad_arguments():
                                     None) == _abi.PR_ERR_INVALID_ARG
     h = C.c_void_p()
     assert lib.pr_stream_create(0, 10, None, C.byref(h)) == _abi.PR_ERR_INVALID_ARG
+    assert lib.pr_stream_create(4, -1, None, C.byref(h)) == _abi.PR_ERR_INVALID_ARG  # 0 = bounded memory
     assert lib.pr_stream_step(None, None, 1, 0, 100, 100, None, None, None, None, None, None) == \
         _abi.PR_ERR_INVALID_ARG
     assert lib.pr_stream_finish(None, None, 1, 0.5, None, None, None) == _abi.PR_ERR_INVALID_ARG
@@ -107,6 +108,18 @@ def test_other_entry_points_reject_bad_arguments():
     feats = _abi.TokenFeatures(*([8] * 10))
     assert lib.pr_token_features(None, 0, 0, 100, 100, None, None, None, C.byref(feats), None, 0, None) == \
         _abi.PR_OK
+
+
+def test_calibrate_rejects_bad_arguments():
+    lib = ensure_built()
+    from paper_2608_28726_amd import _abi
+    p = C.c_void_p(256)
+    bad = _abi.PR_ERR_INVALID_ARG
+    assert lib.pr_calibrate_threshold(p, -1, 0.5, p, p, None) == bad          # n < 0
+    assert lib.pr_calibrate_threshold(None, 4, 0.5, p, p, None) == bad        # no scores
+    assert lib.pr_calibrate_threshold(p, 4, 0.5, None, p, None) == bad        # no tau
+    for q in (-0.1, 1.5, float("nan"), float("inf")):
+        assert lib.pr_calibrate_threshold(p, 4, q, p, p, None) == bad
 
 
 @pytest.mark.parametrize("case", ["k=0", "k>max", "null offsets", "no requests", "null X", "misaligned X",
