@@ -33,10 +33,16 @@ def parse_args():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="ragged_64req_v151936_bf16")
-    ap.add_argument("--path", choices=("features", "sequence", "pipeline"), default="features",
+    ap.add_argument("--path", choices=("features", "sequence", "pipeline", "calibrate"), default="features",
                     help="features: per-token features, per-request summaries and route (the default); "
                          "sequence: the paper's verifier input sequence (l, m, top-20 entropy, t/T) per token; "
-                         "pipeline: that sequence, the paper's transformer head (synthetic weights) and route")
+                         "pipeline: that sequence, the paper's transformer head (synthetic weights) and route; "
+                         "calibrate: the threshold for a ship fraction on a validation pool of --pool scores")
+    ap.add_argument("--pool", type=int, default=8192, help="validation pool size of --path calibrate")
+    ap.add_argument("--ship-fraction", type=float, default=0.7, help="ship fraction of --path calibrate")
+    ap.add_argument("--stream-quantile", choices=("exact", "p2"), default="exact",
+                    help="streaming workloads: exact tail quantile from a per-token history, or the "
+                         "bounded-memory P-square estimate")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="time budget of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
@@ -300,7 +306,7 @@ def run_stream(args, torch, pr, wl, w):
     for p in range(6):  # 6 x 78 MB of distinct step inputs, cycled (above the 256 MB cache)
         pool.append(wl.stream_step_inputs(w, 10_000 + p, np.arange(w.n_req), device="cuda"))
     torch.cuda.synchronize()
-    st = pr.StreamState(w.n_req, n_steps, q=w.q)
+    st = pr.StreamState(w.n_req, n_steps if args.stream_quantile == "exact" else 0, q=w.q)
     actives = [torch.as_tensor(np.flatnonzero(fin >= s).astype(np.int32), device="cuda") for s in range(1, n_steps + 1)]
     endings = [torch.as_tensor(np.flatnonzero(fin == s).astype(np.int32), device="cuda") for s in range(1, n_steps + 1)]
     rows = int(sum(a.shape[0] for a in actives))
@@ -408,6 +414,56 @@ def run_stream(args, torch, pr, wl, w):
     return None, None, rows, pass_ms * 1e-3, kern_full, bytes_step, extra
 
 
+def run_calibrate(args, torch, pr, wl):
+    """Threshold calibration on a validation pool (pr_calibrate_threshold):
+    one call per step, each bracketed by HIP events on the stream it is
+    launched on; the oracle's calibration of the same pool is timed on the
+    host and must give the same tau and ship count."""
+    import oracle
+    n, q = args.pool, args.ship_fraction
+    host = wl.validation_scores(n)
+    s = torch.from_numpy(host).cuda()
+    for _ in range(max(1, args.warmup)):
+        tau, ns = pr.calibrate_threshold(s, q)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for a, b in ev:
+        a.record()
+        tau, ns = pr.calibrate_threshold(s, q)
+        b.record()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    call_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    c0 = time.perf_counter()
+    reps = 0
+    while True:
+        otau, ons = oracle.calibrate_threshold(host.astype(np.float64), q)
+        reps += 1
+        if time.perf_counter() - c0 >= min(args.cpu_seconds, 2.0):
+            break
+    cpu_s = (time.perf_counter() - c0) / reps
+    if float(tau.item()) != otau or int(ns.item()) != ons:
+        raise RuntimeError(f"calibration differs from the oracle: {tau.item()} {ns.item()} vs {otau} {ons}")
+    achieved = 4.0 * n / (call_ms * 1e-3) / 1e9
+    result = {
+        "metric": "threshold calibrations/sec on a validation pool",
+        "value": args.steps / elapsed, "unit": "calibrations/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": elapsed * 1e3 / args.steps, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"validation pool of {n} scores ~ Beta(5,2), 0.5% NaN", "pool": n,
+                   "ship_fraction": q},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None, "kernel": "calibrate_kernel",
+                     "kernel_ms": call_ms, "bytes_per_launch": 4 * n},
+        "cpu_baseline": {"value": 1.0 / cpu_s, "unit": "calibrations/s", "cores": 1, "kind": "oracle",
+                         "sample": f"the same pool, {reps} calibrations"},
+        "tau": float(tau.item()), "n_ship": int(ns.item()),
+    }
+    log(f"[bench] calibrate: {n} scores, {call_ms * 1e3:.1f} us per call; oracle {cpu_s * 1e3:.2f} ms")
+    print(json.dumps(result), flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -419,6 +475,9 @@ def main():
     import paper_2608_28726_amd as pr
     from paper_2608_28726_amd import workloads as wl
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.path == "calibrate":
+        run_calibrate(args, torch, pr, wl)
+        return
 
     w = wl.WORKLOADS[args.workload]
     log(f"[bench] generating {w.name} on the GPU")
@@ -459,7 +518,9 @@ def main():
                             "pipeline": "verifier input sequence, transformer head (synthetic weights), route"}.get(
                                 args.path, "features, summaries, route"),
                    "temperature": [w.T_lo, w.T_hi], "top_p": None if w.P_lo is None else [w.P_lo, w.P_hi],
-                   "aggregation": f"mean/min/q={w.q} nearest-rank", "threshold": w.tau},
+                   "aggregation": (f"mean/min/q={w.q} P-square estimate" if stream_mode and
+                                   args.stream_quantile == "p2" else f"mean/min/q={w.q} nearest-rank"),
+                   "threshold": w.tau},
         "gb_per_s": achieved,
         "pct_of_hbm_peak": 100.0 * achieved / HBM_PEAK_GBS,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -482,7 +543,8 @@ def main():
 KERNEL_SOURCES = {
     "row_features_kernel": ("include/prouter.h", "paper_2608_28726_amd/csrc/device_util.h",
                             "paper_2608_28726_amd/csrc/row_features.h", "paper_2608_28726_amd/csrc/row_scan.h",
-                            "paper_2608_28726_amd/csrc/topk.h", "paper_2608_28726_amd/csrc/row_features.hip"),
+                            "paper_2608_28726_amd/csrc/topk.h", "paper_2608_28726_amd/csrc/p2.h",
+                            "paper_2608_28726_amd/csrc/row_features.hip"),
     "topp_kernel": ("include/prouter.h", "paper_2608_28726_amd/csrc/device_util.h",
                     "paper_2608_28726_amd/csrc/row_features.h", "paper_2608_28726_amd/csrc/row_scan.h",
                     "paper_2608_28726_amd/csrc/topk.h", "paper_2608_28726_amd/csrc/topp.h",

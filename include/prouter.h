@@ -251,10 +251,17 @@ pr_status pr_route(const float* scores, int32_t n_req, float threshold, uint8_t*
  * #{scores >= tau}, at least k (more when scores tie at tau). -0 counts as
  * +0. ship_fraction == 0 or no valid score: tau = +inf, n_ship = 0.
  * ship_fraction must lie in [0, 1] (NaN rejected); n >= 0; scores may be
- * NULL only when n == 0. Exact: tau is one of the scores.
+ * NULL only when n == 0. Exact: tau is one of the scores. workspace: device
+ * memory of at least pr_calibrate_workspace(n) bytes, 4-byte aligned, owned
+ * by the caller and not shared with a concurrent call (NULL when that size
+ * is 0: pools of up to 16,384 scores need none); otherwise
+ * PR_ERR_INVALID_ARG.
  */
 pr_status pr_calibrate_threshold(const float* scores, int32_t n, double ship_fraction, float* tau, int32_t* n_ship,
-                                 void* stream);
+                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes pr_calibrate_threshold needs for a pool of n scores (0 for n <= 16,384). */
+size_t pr_calibrate_workspace(int32_t n);
 
 /*
  * Synchronous debug check of an offsets array (device pointer): returns

@@ -229,10 +229,13 @@ def calibrate_threshold(scores: torch.Tensor, ship_fraction: float):
     (``pr_calibrate_threshold``). Returns (tau float32 [1], n_ship int32 [1])."""
     if scores.dtype != torch.float32 or not scores.is_cuda or not scores.is_contiguous() or scores.dim() != 1:
         raise ValueError("scores must be a 1-D contiguous float32 CUDA tensor")
+    n = scores.shape[0]
     tau = torch.empty(1, dtype=torch.float32, device=scores.device)
     n_ship = torch.empty(1, dtype=torch.int32, device=scores.device)
-    st = _abi.lib().pr_calibrate_threshold(_ptr(scores), scores.shape[0], float(ship_fraction), _ptr(tau),
-                                          _ptr(n_ship), _stream_handle())
+    ws_bytes = _abi.lib().pr_calibrate_workspace(n)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=scores.device) if ws_bytes else None
+    st = _abi.lib().pr_calibrate_threshold(_ptr(scores), n, float(ship_fraction), _ptr(tau), _ptr(n_ship),
+                                          _ptr(ws), ws_bytes, _stream_handle())
     _abi.check("pr_calibrate_threshold", st)
     return tau, n_ship
 

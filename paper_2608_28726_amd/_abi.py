@@ -24,6 +24,7 @@ EXPORTED = (
     "pr_request_aggregate", "pr_route", "pr_validate_offsets", "pr_stream_create", "pr_stream_step",
     "pr_stream_finish", "pr_stream_reset_slots", "pr_stream_destroy", "pr_feature_sequence",
     "pr_verifier_head_workspace", "pr_verifier_head", "pr_calibrate_threshold",
+    "pr_calibrate_workspace",
 )
 
 PR_HEAD_WEIGHTS = 67329
@@ -83,8 +84,10 @@ def lib() -> C.CDLL:
     L.pr_request_aggregate.restype = C.c_int
     L.pr_route.argtypes = [vp, i32, f32, vp, vp, vp]
     L.pr_route.restype = C.c_int
-    L.pr_calibrate_threshold.argtypes = [vp, i32, C.c_double, vp, vp, vp]
+    L.pr_calibrate_threshold.argtypes = [vp, i32, C.c_double, vp, vp, vp, C.c_size_t, vp]
     L.pr_calibrate_threshold.restype = C.c_int
+    L.pr_calibrate_workspace.argtypes = [i32]
+    L.pr_calibrate_workspace.restype = C.c_size_t
     L.pr_validate_offsets.argtypes = [vp, i32, i64, vp]
     L.pr_validate_offsets.restype = C.c_int
     L.pr_stream_create.argtypes = [i32, i32, C.POINTER(AggParams), C.POINTER(vp)]

@@ -193,11 +193,16 @@ pr_status pr_route(const float* scores, int32_t n_req, float threshold, uint8_t*
   return hip_status(launch_route(scores, n_req, threshold, ship, n_ship, as_stream(stream)));
 }
 
+size_t pr_calibrate_workspace(int32_t n) { return n < 0 ? 0 : calibrate_workspace_bytes(n); }
+
 pr_status pr_calibrate_threshold(const float* scores, int32_t n, double ship_fraction, float* tau, int32_t* n_ship,
-                                 void* stream) {
+                                 void* workspace, size_t workspace_bytes, void* stream) {
   if (n < 0 || !tau || (n > 0 && !scores)) return PR_ERR_INVALID_ARG;
   if (!(ship_fraction >= 0.0 && ship_fraction <= 1.0)) return PR_ERR_INVALID_ARG;
-  return hip_status(launch_calibrate(scores, n, ship_fraction, tau, n_ship, as_stream(stream)));
+  const size_t need = calibrate_workspace_bytes(n);
+  if (need && (!workspace || workspace_bytes < need || reinterpret_cast<uintptr_t>(workspace) % 4 != 0))
+    return PR_ERR_INVALID_ARG;
+  return hip_status(launch_calibrate(scores, n, ship_fraction, tau, n_ship, workspace, as_stream(stream)));
 }
 
 pr_status pr_validate_offsets(const int32_t* offsets, int32_t n_req, int64_t n_rows, void* stream) {

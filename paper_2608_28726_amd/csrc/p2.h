@@ -50,11 +50,32 @@ __device__ __forceinline__ void sort5(double* v) {
   }
 }
 
-// Feeds one observation of column f to the slot's markers.
-__device__ void feed(const StreamDev& s, int32_t slot, int f, float v) {
+// One column's marker state as read from memory.
+struct Markers {
+  double q[5];
+  int32_t n1, n2, n3, fed;
+};
+
+__device__ __forceinline__ Markers load(const StreamDev& s, int32_t slot, int f) {
+  const int32_t* nb = positions(s, slot, f);
+  const double* qb = heights(s, slot, f);
+  Markers m;
+#pragma unroll
+  for (int i = 0; i < 5; ++i) m.q[i] = qb[4 * i];
+  m.n1 = nb[0];
+  m.n2 = nb[4];
+  m.n3 = nb[8];
+  m.fed = nb[12];
+  return m;
+}
+
+// Feeds one observation of column f to the slot's markers, whose state m was
+// read before (nothing else changes it meanwhile: a slot takes at most one
+// token per step).
+__device__ void feed(const StreamDev& s, int32_t slot, int f, float v, const Markers& m) {
   int32_t* nb = positions(s, slot, f);
   double* qb = heights(s, slot, f);
-  const int32_t fed = nb[12];
+  const int32_t fed = m.fed;
   if (fed < 0 || v != v) return;
   if (__builtin_isinf(v)) {
     nb[12] = -1;
@@ -68,7 +89,7 @@ __device__ void feed(const StreamDev& s, int32_t slot, int f, float v) {
       qb[4 * (N - 1)] = x;
       return;
     }
-    double q[5] = {qb[0], qb[4], qb[8], qb[12], x};
+    double q[5] = {m.q[0], m.q[1], m.q[2], m.q[3], x};
     sort5(q);
 #pragma unroll
     for (int i = 0; i < 5; ++i) qb[4 * i] = q[i];
@@ -80,11 +101,11 @@ __device__ void feed(const StreamDev& s, int32_t slot, int f, float v) {
   double q[5];
   int32_t n[5];
 #pragma unroll
-  for (int i = 0; i < 5; ++i) q[i] = qb[4 * i];
+  for (int i = 0; i < 5; ++i) q[i] = m.q[i];
   n[0] = 1;
-  n[1] = nb[0];
-  n[2] = nb[4];
-  n[3] = nb[8];
+  n[1] = m.n1;
+  n[2] = m.n2;
+  n[3] = m.n3;
   n[4] = N - 1;
   // The cell k with q_k <= x < q_(k+1); the extreme markers follow the
   // extremes. The heights stay ordered, so the cell is the number of
@@ -129,10 +150,30 @@ __device__ void feed(const StreamDev& s, int32_t slot, int f, float v) {
   nb[8] = n[3];
 }
 
+// The slot of row r when its markers are to be fed (streaming in
+// bounded-memory mode), else -1.
+__device__ __forceinline__ int32_t row_slot(const RowArgs& a, int64_t r) {
+  if (!a.slot_ids || !a.st.p2q) return -1;
+  const int32_t slot = a.slot_ids[r];
+  return slot >= 0 && slot < a.st.max_slots ? slot : -1;
+}
+
+// Lane f < 4 of the finalising wave reads column f's markers of row r's slot
+// (early, so that the latency hides behind the row).
+struct RowMarkers {
+  int32_t slot;
+  Markers m;
+  __device__ __forceinline__ void fetch(const RowArgs& a, int64_t r) {
+    slot = row_slot(a, r);
+    const int lane = threadIdx.x % kWave;
+    if (slot >= 0 && lane < 4) m = load(a.st, slot, lane);
+  }
+};
+
 // The row's token joins its slot's markers: the confidence tuple is held by
-// lane 0 of the calling wave, lanes 0..3 feed columns 0..3. Every lane of the
-// wave must call this.
-__device__ __forceinline__ void feed_row(const RowArgs& a, int64_t r, const float* conf) {
+// lane 0 of the calling wave, lanes 0..3 feed columns 0..3 from the state
+// fetched before. Every lane of the wave must call this.
+__device__ __forceinline__ void feed_row(const RowArgs& a, const RowMarkers& rm, const float* conf) {
   const int lane = threadIdx.x % kWave;
   float v = 0.0f;
 #pragma unroll
@@ -140,10 +181,7 @@ __device__ __forceinline__ void feed_row(const RowArgs& a, int64_t r, const floa
     const float t = __shfl(conf[f], 0);
     if (lane == f) v = t;
   }
-  if (lane < 4) {
-    const int32_t slot = a.slot_ids[r];
-    if (slot >= 0 && slot < a.st.max_slots) feed(a.st, slot, lane, v);
-  }
+  if (rm.slot >= 0 && lane < 4) feed(a.st, rm.slot, lane, v, rm.m);
 }
 
 // The estimate of column f: NaN when nothing was fed or an infinite value

@@ -60,7 +60,11 @@ void row_features_kernel(RowArgs a) {
   // other workgroups on the CU cover it and no registers stay tied up.
   constexpr bool kEarlySlot = !SPLIT && BLOCK >= 512;
   SlotState ss{-1};
-  if (kEarlySlot) ss = slot_load(a, r);
+  p2::RowMarkers pm;
+  if (kEarlySlot) {
+    ss = slot_load(a, r);
+    if (threadIdx.x < kWave) pm.fetch(a, r);
+  }
 
   Lane L;
   lane_init(L);
@@ -95,12 +99,13 @@ void row_features_kernel(RowArgs a) {
     return;
   }
   if (threadIdx.x < kWave) {
+    if (!kEarlySlot) pm.fetch(a, r);
     float conf[4];
     if (threadIdx.x == 0) {
       finalize_row(a, r, p, cx, fix, conf);
       stream_update(a.st, kEarlySlot ? ss : slot_load(a, r), conf);
     }
-    if (a.slot_ids && a.st.p2q) p2::feed_row(a, r, conf);
+    if (pm.slot >= 0) p2::feed_row(a, pm, conf);
   }
 }
 
@@ -128,6 +133,8 @@ __global__ __launch_bounds__(kWave) void row_merge_kernel(RowArgs a) {
   }
   const RowMeta meta = split_meta(a.ws, a.n_rows, G)[r];
   const SlotState ss = slot_load(a, r);
+  p2::RowMarkers pm;
+  pm.fetch(a, r);
   RowCtx cx;
   cx.T = meta.T;
   cx.c = temperature_ok(meta.T) ? kLog2e / meta.T : kLog2e;
@@ -153,7 +160,7 @@ __global__ __launch_bounds__(kWave) void row_merge_kernel(RowArgs a) {
     finalize_row(a, r, p, cx, meta.fix, conf);
     stream_update(a.st, ss, conf);
   }
-  if (a.slot_ids && a.st.p2q) p2::feed_row(a, r, conf);
+  if (pm.slot >= 0) p2::feed_row(a, pm, conf);
 }
 
 namespace {

@@ -241,3 +241,13 @@ def head_weights(seed: int = 0x50524844) -> np.ndarray:
             v = rng.uniform(-a, a, n)
         parts.append(v.astype(np.float32))
     return np.concatenate(parts)
+
+
+def validation_scores(n: int, seed: int = 0x50524341, nan_frac: float = 0.005) -> np.ndarray:
+    """A seeded validation pool of n shipping confidences in (0, 1), skewed
+    towards confident requests (Beta(5, 2)), with a fraction of NaN (requests
+    without a score). float32."""
+    rng = np.random.default_rng(seed)
+    s = rng.beta(5.0, 2.0, n).astype(np.float32)
+    s[rng.random(n) < nan_frac] = np.nan
+    return s

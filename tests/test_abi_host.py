@@ -115,11 +115,17 @@ def test_calibrate_rejects_bad_arguments():
     from paper_2608_28726_amd import _abi
     p = C.c_void_p(256)
     bad = _abi.PR_ERR_INVALID_ARG
-    assert lib.pr_calibrate_threshold(p, -1, 0.5, p, p, None) == bad          # n < 0
-    assert lib.pr_calibrate_threshold(None, 4, 0.5, p, p, None) == bad        # no scores
-    assert lib.pr_calibrate_threshold(p, 4, 0.5, None, p, None) == bad        # no tau
+    assert lib.pr_calibrate_threshold(p, -1, 0.5, p, p, None, 0, None) == bad          # n < 0
+    assert lib.pr_calibrate_threshold(None, 4, 0.5, p, p, None, 0, None) == bad        # no scores
+    assert lib.pr_calibrate_threshold(p, 4, 0.5, None, p, None, 0, None) == bad        # no tau
     for q in (-0.1, 1.5, float("nan"), float("inf")):
-        assert lib.pr_calibrate_threshold(p, 4, q, p, p, None) == bad
+        assert lib.pr_calibrate_threshold(p, 4, q, p, p, None, 0, None) == bad
+    assert lib.pr_calibrate_workspace(16384) == 0 and lib.pr_calibrate_workspace(-5) == 0
+    need = lib.pr_calibrate_workspace(16385)
+    assert need > 0 and lib.pr_calibrate_workspace(1 << 30) == need
+    assert lib.pr_calibrate_threshold(p, 16385, 0.5, p, p, None, need, None) == bad    # no workspace
+    assert lib.pr_calibrate_threshold(p, 16385, 0.5, p, p, p, need - 4, None) == bad   # too small
+    assert lib.pr_calibrate_threshold(p, 16385, 0.5, p, p, C.c_void_p(258), need, None) == bad  # misaligned
 
 
 @pytest.mark.parametrize("case", ["k=0", "k>max", "null offsets", "no requests", "null X", "misaligned X",
