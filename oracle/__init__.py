@@ -17,12 +17,14 @@ ship rule p >= tau):
 * :mod:`oracle.head` -- the paper's verifier head over that input:
   projection with positional encoding, two post-norm encoder layers, mean
   pool and sigmoid (run with seeded synthetic weights).
+* :mod:`oracle.sampling` -- the distribution the fused sample-and-verify
+  path draws each token from.
 * :mod:`oracle.calibrate` -- the threshold tau for a ship fraction on a
   validation pool, and the P-square streaming quantile (bounded memory).
 
 Parity pinning: every function here is pinned by ``tests/test_oracle_pins.py``,
-``tests/test_oracle_sequence.py``, ``tests/test_oracle_head.py`` and
-``tests/test_oracle_calibrate.py`` against
+``tests/test_oracle_sequence.py``, ``tests/test_oracle_head.py``,
+``tests/test_oracle_calibrate.py`` and ``tests/test_oracle_sampling.py`` against
 closed forms, invariants, pure-Python brute force and (for the head) an
 independent implementation of the same architecture, except the default
 score head (a fixed linear summary chosen because the paper publishes no
@@ -54,3 +56,4 @@ from .sequence import (  # noqa: F401
 )
 from .head import HEAD_WEIGHTS, head_score, head_scores  # noqa: F401,E402
 from .calibrate import P2Quantile, calibrate_threshold, p2_quantile  # noqa: F401,E402
+from .sampling import token_probabilities  # noqa: F401,E402
