@@ -33,10 +33,12 @@ def parse_args():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="ragged_64req_v151936_bf16")
-    ap.add_argument("--path", choices=("features", "sequence", "pipeline", "calibrate"), default="features",
+    ap.add_argument("--path", choices=("features", "sample", "sequence", "pipeline", "calibrate"), default="features",
                     help="features: per-token features, per-request summaries and route (the default); "
                          "sequence: the paper's verifier input sequence (l, m, top-20 entropy, t/T) per token; "
                          "pipeline: that sequence, the paper's transformer head (synthetic weights) and route; "
+                         "sample: each row's token drawn in the same pass as its features (fused "
+                         "sample-and-verify), then summaries and route; "
                          "calibrate: the threshold for a ship fraction on a validation pool of --pool scores")
     ap.add_argument("--pool", type=int, default=8192, help="validation pool size of --path calibrate")
     ap.add_argument("--ship-fraction", type=float, default=0.7, help="ship fraction of --path calibrate")
@@ -135,8 +137,9 @@ def cpu_baseline_sequence(torch, batch, X_gpu, seconds, top_k):
     }
 
 
-def cpu_baseline(torch, batch, feats_gpu, seconds):
-    """The fp64 oracle on the first rows of the batch, time-bounded, one core."""
+def cpu_baseline(torch, batch, feats_gpu, seconds, skip=()):
+    """The fp64 oracle on the first rows of the batch, time-bounded, one core
+    (the features named in skip are not compared)."""
     import oracle
     from oracle import aggregate as oagg
     from paper_2608_28726_amd import workloads as wl
@@ -173,6 +176,8 @@ def cpu_baseline(torch, batch, feats_gpu, seconds):
             i = np.flatnonzero(~ok)[:3]
             detail[k] = {"count": int((~ok).sum()), "rows": i.tolist(), "gpu": g[i].tolist(), "oracle": o[i].tolist()}
     for k in ("rank", "argmax", "cutoff"):
+        if k in skip:
+            continue
         g = feats_gpu[k][:n].cpu().numpy()
         o = np.array([d[k] for d in res])
         bad += int((g != o).sum())
@@ -218,6 +223,8 @@ def run_offline(args, torch, pr, wl, w):
     offs = [torch.as_tensor(b.offsets).cuda() for b in batches]
     sequence = args.path in ("sequence", "pipeline")
     pipeline = args.path == "pipeline"
+    sample = args.path == "sample"
+    drawn = [torch.empty(b.n_rows, dtype=torch.int32, device="cuda") for b in batches] if sample else None
     if pipeline:
         head_w = torch.tensor(wl.head_weights(), device="cuda")
         head_ws = [torch.empty(max(int(pr._abi.lib().pr_verifier_head_workspace(b.n_rows)), 1), dtype=torch.uint8,
@@ -244,6 +251,9 @@ def run_offline(args, torch, pr, wl, w):
             if sequence:
                 pr.feature_sequence(b.logits, b.sampled_ids, b.temperature, offs[c], top_p=b.top_p,
                                     top_k=pr.PAPER_TOP_K, out=feats[c])
+            elif sample:
+                pr.sample_features(b.logits, b.temperature, seed=20261202, offset=state["k"], ids_out=drawn[c],
+                                   out=feats[c])
             else:
                 pr.token_features(b.logits, b.sampled_ids, b.temperature, b.top_p, out=feats[c],
                                   workspace=wss[c])
@@ -280,6 +290,8 @@ def run_offline(args, torch, pr, wl, w):
     kernel = "topp_kernel" if w.P_lo is not None else "row_features_kernel"
     if sequence:
         kernel += " (sequence variant)"
+    if sample:
+        kernel += " (sampling variant)"
     if n_chunks > 1:  # events bracket all chunks' row kernels and their summaries
         kernel += f" x{n_chunks} chunks (+summaries)"
     extra = {"kernel": kernel, "kernel_ms": kern_ms, "bytes_per_launch": bytes_launch}
@@ -289,6 +301,12 @@ def run_offline(args, torch, pr, wl, w):
         extra["head"] = {"ms": head_ms, "gflop": flops / 1e9, "tflop_per_s": flops / (head_ms * 1e-3) / 1e12,
                          "peak_tflop_per_s": MFMA_F32_PEAK_TFLOPS, "weights": "synthetic (seeded)"}
         log(f"[bench] verifier head {head_ms * 1e3:.1f} us per batch, {flops / 1e9:.2f} GFLOP")
+    if sample:  # the oracle baseline checks the drawn rows' features for the drawn ids
+        b = batches[0]
+        pr.sample_features(b.logits, b.temperature, seed=20261202, offset=0, ids_out=drawn[0], out=feats[0])
+        torch.cuda.synchronize()
+        return (wl.Batch(b.workload, b.offsets, b.logits, drawn[0], b.temperature, b.top_p), feats[0], n_rows,
+                elapsed, kern_ms, bytes_launch, extra)
     return batches[0], feats[0], n_rows, elapsed, kern_ms, bytes_launch, extra
 
 
@@ -515,7 +533,9 @@ def main():
         "config": {"workload": w.name, "n_req": w.n_req, "rows": n_rows, "V": w.V, "logits": w.dtype,
                    "mode": "streaming decode, one step per token" if stream_mode else "offline ragged batch",
                    "path": {"sequence": "verifier input sequence (l, m, top-20 entropy, t/T)",
-                            "pipeline": "verifier input sequence, transformer head (synthetic weights), route"}.get(
+                            "pipeline": "verifier input sequence, transformer head (synthetic weights), route",
+                            "sample": "token drawn in the same pass (fused sample-and-verify), features, "
+                                      "summaries, route"}.get(
                                 args.path, "features, summaries, route"),
                    "temperature": [w.T_lo, w.T_hi], "top_p": None if w.P_lo is None else [w.P_lo, w.P_hi],
                    "aggregation": (f"mean/min/q={w.q} P-square estimate" if stream_mode and
@@ -533,7 +553,8 @@ def main():
         if args.path in ("sequence", "pipeline"):
             result["cpu_baseline"] = cpu_baseline_sequence(torch, batch, feats, args.cpu_seconds, pr.PAPER_TOP_K)
         else:
-            result["cpu_baseline"] = cpu_baseline(torch, batch, feats, args.cpu_seconds)
+            result["cpu_baseline"] = cpu_baseline(torch, batch, feats, args.cpu_seconds,
+                                                  skip=("rank",) if args.path == "sample" else ())
         log(f"[bench] oracle {result['cpu_baseline']['value']:.1f} rows/s, "
             f"parity mismatches {result['cpu_baseline']['parity_mismatches']}")
     print(json.dumps(result), flush=True)

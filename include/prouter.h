@@ -182,6 +182,43 @@ pr_status pr_feature_sequence(const void* logits, pr_dtype dtype, int64_t n_rows
                               const float* top_p, const int32_t* offsets, int32_t n_req, int32_t top_k,
                               float* X, const pr_token_features_t* features, void* stream);
 
+/*
+ * Fused sample-and-verify (the verifier reads the decoding distribution as a
+ * side product of decoding, Sec. 3.1 and Sec. 4.1): one read of each row both
+ * draws its token y_r from softmax(z_r / T_r) and computes the verifier's
+ * outputs for that token.
+ *   logits, dtype, n_rows, vocab, row_stride, temperature
+ *              as for pr_token_features (no top-p).
+ *   seed, offset
+ *              the draw is a fixed function of (seed, offset, row index, the
+ *              row's logits and temperature, and the workgroup size, which
+ *              the number of rows selects: at least 2,048, 257..2,047, or up
+ *              to 256): the same call gives the same tokens; a new offset
+ *              (e.g. the decode step) gives fresh draws. Uniforms come from
+ *              Threefry-2x32-13 (Salmon et al., SC 2011).
+ *   sampled_ids
+ *              int32 [n_rows], device, written: the drawn token, or -1 when
+ *              the row's distribution is undefined (non-finite logits or a
+ *              rejected temperature). A token of probability 0 is never
+ *              drawn. Each token v is drawn with probability e_v / S up to
+ *              float32 rounding of the masses (relative 1e-6).
+ *   features   host pointer to a struct of device arrays (all members set),
+ *              or NULL: the per-token features of pr_token_features for the
+ *              drawn token, except rank, which is written as 0 (counting
+ *              the tokens above y needs z_y before the pass); a row with y =
+ *              -1 is flagged PR_FLAG_BAD_ID besides its other flags.
+ *   offsets, n_req, top_k, X
+ *              X NULL: not computed. Otherwise the paper's verifier input
+ *              sequence for the drawn tokens, with the arguments and layout
+ *              of pr_feature_sequence.
+ * One workgroup reads each row once; no workspace. n_rows == 0 launches
+ * nothing.
+ */
+pr_status pr_sample_features(const void* logits, pr_dtype dtype, int64_t n_rows, int32_t vocab, int64_t row_stride,
+                             const float* temperature, uint64_t seed, uint64_t offset, int32_t* sampled_ids,
+                             const pr_token_features_t* features, const int32_t* offsets, int32_t n_req,
+                             int32_t top_k, float* X, void* stream);
+
 /* The verifier head (Sec. 3.1, the paragraph after Eq. 3; Sec. 4.2): its
  * number of float32 parameters, and the device workspace it needs. */
 #define PR_HEAD_WEIGHTS 67329

@@ -25,7 +25,7 @@ from . import _abi
 from ._abi import (FLAG_BAD_ID, FLAG_BAD_TP, FLAG_NONFINITE, FLAG_OUTSIDE_NUCLEUS,  # noqa: F401
                    ProuterError)
 
-__all__ = ["token_features", "feature_sequence", "verifier_head", "request_aggregate", "route", "calibrate_threshold",
+__all__ = ["token_features", "feature_sequence", "sample_features", "verifier_head", "request_aggregate", "route", "calibrate_threshold",
            "validate_offsets", "StreamState",
            "token_features_workspace", "ProuterError", "FEATURE_FLOATS", "FEATURE_INTS", "PAPER_TOP_K"]
 
@@ -140,6 +140,46 @@ def feature_sequence(logits: torch.Tensor, sampled_ids: torch.Tensor, temperatur
                                         offsets.shape[0] - 1, int(top_k), _ptr(X), fs, _stream_handle())
     _abi.check("pr_feature_sequence", st)
     return (X, feats) if features else X
+
+
+def sample_features(logits: torch.Tensor, temperature, seed: int, offset: int = 0, features: bool = True,
+                    offsets: torch.Tensor | None = None, top_k: int = PAPER_TOP_K, ids_out: torch.Tensor | None = None,
+                    out: dict | None = None):
+    """Fused sample-and-verify (``pr_sample_features``): draws each row's token
+    from softmax(logits / T) in the same pass that computes its features.
+
+    Returns ``(ids, feats, X)``: the drawn tokens (int32 [n_rows], -1 where the
+    distribution is undefined), the per-token features for them as
+    :func:`token_features` returns them (rank written as 0), or None with
+    ``features=False``, and the paper's input sequence X for them when
+    ``offsets`` is given (else None). The draw is a fixed function of
+    (seed, offset, row index, logits, temperature) and of the workgroup size
+    the number of rows selects. ``ids_out`` / ``out``: optional preallocated
+    outputs (int32 [n_rows]; a features dict as :func:`token_features`
+    returns)."""
+    n, V = logits.shape
+    temperature = _as_row_tensor(temperature, n, logits.device)
+    if logits.dim() != 2 or not logits.is_cuda or logits.stride(1) != 1:
+        raise ValueError("logits must be a 2-D CUDA tensor with unit column stride")
+    if logits.dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("logits must be float32 or bfloat16")
+    ids = torch.empty(n, dtype=torch.int32, device=logits.device) if ids_out is None else ids_out
+    if ids.dtype != torch.int32 or ids.shape != (n,) or not ids.is_contiguous() or ids.device != logits.device:
+        raise ValueError(f"ids_out must be a contiguous int32 [{n}] tensor on {logits.device}")
+    feats = (out if out is not None else _alloc_features(n, logits.device)) if features else None
+    fs = C.byref(_features_struct(feats)) if feats is not None else None
+    X = None
+    n_req = 0
+    if offsets is not None:
+        if offsets.dtype != torch.int32 or not offsets.is_cuda or offsets.dim() != 1 or not offsets.is_contiguous():
+            raise ValueError("offsets must be a contiguous 1-D int32 CUDA tensor")
+        X = torch.empty(n, 4, dtype=torch.float32, device=logits.device)
+        n_req = offsets.shape[0] - 1
+    st = _abi.lib().pr_sample_features(_ptr(logits), _dtype_code(logits), n, V, logits.stride(0), _ptr(temperature),
+                                       int(seed) & 0xFFFFFFFFFFFFFFFF, int(offset) & 0xFFFFFFFFFFFFFFFF, _ptr(ids),
+                                       fs, _ptr(offsets), n_req, int(top_k), _ptr(X), _stream_handle())
+    _abi.check("pr_sample_features", st)
+    return ids, feats, X
 
 
 def verifier_head(X: torch.Tensor, offsets: torch.Tensor, weights: torch.Tensor, max_len: int | None = None,

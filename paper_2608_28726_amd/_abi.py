@@ -24,7 +24,7 @@ EXPORTED = (
     "pr_request_aggregate", "pr_route", "pr_validate_offsets", "pr_stream_create", "pr_stream_step",
     "pr_stream_finish", "pr_stream_reset_slots", "pr_stream_destroy", "pr_feature_sequence",
     "pr_verifier_head_workspace", "pr_verifier_head", "pr_calibrate_threshold",
-    "pr_calibrate_workspace",
+    "pr_calibrate_workspace", "pr_sample_features",
 )
 
 PR_HEAD_WEIGHTS = 67329
@@ -86,6 +86,9 @@ def lib() -> C.CDLL:
     L.pr_route.restype = C.c_int
     L.pr_calibrate_threshold.argtypes = [vp, i32, C.c_double, vp, vp, vp, C.c_size_t, vp]
     L.pr_calibrate_threshold.restype = C.c_int
+    L.pr_sample_features.argtypes = [vp, C.c_int, i64, i32, i64, vp, C.c_uint64, C.c_uint64, vp,
+                                     C.POINTER(TokenFeatures), vp, i32, i32, vp, vp]
+    L.pr_sample_features.restype = C.c_int
     L.pr_calibrate_workspace.argtypes = [i32]
     L.pr_calibrate_workspace.restype = C.c_size_t
     L.pr_validate_offsets.argtypes = [vp, i32, i64, vp]

@@ -150,6 +150,40 @@ pr_status pr_feature_sequence(const void* logits, pr_dtype dtype, int64_t n_rows
   return hip_status(launch_feature_sequence(a, dtype, as_stream(stream)));
 }
 
+pr_status pr_sample_features(const void* logits, pr_dtype dtype, int64_t n_rows, int32_t vocab, int64_t row_stride,
+                             const float* temperature, uint64_t seed, uint64_t offset, int32_t* sampled_ids,
+                             const pr_token_features_t* features, const int32_t* offsets, int32_t n_req,
+                             int32_t top_k, float* X, void* stream) {
+  if (dtype != PR_F32 && dtype != PR_BF16) return PR_ERR_INVALID_ARG;
+  if (n_rows < 0 || vocab < 2 || row_stride < vocab) return PR_ERR_INVALID_ARG;
+  if (n_rows > (int64_t{1} << 26)) return PR_ERR_UNSUPPORTED;
+  if (features && !features_complete(features)) return PR_ERR_INVALID_ARG;
+  if (X && (top_k < 1 || top_k > PR_MAX_TOP_K || n_req < 0)) return PR_ERR_INVALID_ARG;
+  if (n_rows == 0) return PR_OK;
+  if (!logits || !temperature || !sampled_ids || !aligned(logits, dtype_size(dtype))) return PR_ERR_INVALID_ARG;
+  if (X && (n_req == 0 || !offsets || !aligned(X, 16))) return PR_ERR_INVALID_ARG;
+  RowArgs a{};
+  a.logits = logits;
+  a.n_rows = n_rows;
+  a.V = vocab;
+  a.row_stride = row_stride;
+  a.sampled_ids = nullptr;
+  a.temperature = temperature;
+  if (features) a.out = *features;
+  a.G = 1;
+  a.X = X;
+  a.offsets = offsets;
+  a.n_req = n_req;
+  a.top_k = top_k;
+  a.sampled_out = sampled_ids;
+  // One key per (seed, offset): the offset is spread by an odd multiplier
+  // (a bijection of 64-bit words), so each offset gives its own key.
+  const uint64_t key = seed ^ (offset * 0x9E3779B97F4A7C15ull);
+  a.key0 = static_cast<uint32_t>(key);
+  a.key1 = static_cast<uint32_t>(key >> 32);
+  return hip_status(launch_sample(a, dtype, as_stream(stream)));
+}
+
 size_t pr_verifier_head_workspace(int64_t n_rows) { return n_rows > 0 ? head_workspace_bytes(n_rows) : 0; }
 
 pr_status pr_verifier_head(const float* X, int64_t n_rows, const int32_t* offsets, int32_t n_req, int32_t max_len,

@@ -48,6 +48,9 @@ struct RowArgs {
   const int32_t* offsets;   // [n_req + 1] request boundaries
   int32_t n_req;
   int32_t top_k;            // K of the top-K entropy, 1..topk::kMaxK
+  // Fused sampling (sampled_ids NULL): the drawn token of each row.
+  int32_t* sampled_out;     // [n_rows]
+  uint32_t key0, key1;      // generator key from the caller's seed and offset
 };
 
 // Workgroups per row chosen for a shape (the same in every call, so that the
@@ -71,5 +74,10 @@ hipError_t launch_row_features(const RowArgs& a, pr_dtype dtype, hipStream_t str
 // The verifier input sequence X (with the features when a.out is set): one
 // workgroup per row, no split.
 hipError_t launch_feature_sequence(const RowArgs& a, pr_dtype dtype, hipStream_t stream);
+
+// Fused sample-and-verify: each row's token is drawn in the same pass
+// (a.sampled_out), then its features (a.out, when set) and row of X (a.X,
+// when set) are written as for that token. One workgroup per row.
+hipError_t launch_sample(const RowArgs& a, pr_dtype dtype, hipStream_t stream);
 
 }  // namespace pr

@@ -17,6 +17,7 @@
 
 #include "p2.h"
 #include "row_scan.h"
+#include "sample.h"
 #include "topk.h"
 
 namespace pr {
@@ -37,11 +38,14 @@ using namespace scan;
 // so no workgroup waits or fences on another.
 // SEQ == true (one workgroup per row): the row's K largest logits are found
 // in the same pass and row r of the verifier input sequence X is written.
-template <typename Tin, int BLOCK, int U, int LD, bool SPLIT, bool SEQ = false>
+// SAMPLE == true (one workgroup per row): the row's token is drawn in the
+// same pass (sample.h) and the row is finalised for it.
+template <typename Tin, int BLOCK, int U, int LD, bool SPLIT, bool SEQ = false, bool SAMPLE = false>
 __global__ __launch_bounds__(BLOCK)
 __attribute__((amdgpu_waves_per_eu(BLOCK >= 512 ? BLOCK / 256 : PR_ROW_WAVES_PER_EU)))
 void row_features_kernel(RowArgs a) {
   static_assert(!(SPLIT && SEQ), "the sequence variant keeps a row in one workgroup");
+  static_assert(!(SPLIT && SAMPLE), "the sampling variant keeps a row in one workgroup");
   const int G = a.G;
   const int64_t r = blockIdx.x / G;
   const int g = blockIdx.x % G;
@@ -68,8 +72,14 @@ void row_features_kernel(RowArgs a) {
 
   Lane L;
   lane_init(L);
-  typename std::conditional<SEQ, topk::Hook, NoHook>::type hook;
-  if constexpr (SEQ) hook.init();
+  using SeqHook = typename std::conditional<SEQ, topk::Hook, NoHook>::type;
+  typename std::conditional<SAMPLE, HookPair<sample::Hook, SeqHook>, SeqHook>::type hook;
+  SeqHook& seq_hook = [&]() -> SeqHook& {
+    if constexpr (SAMPLE) return hook.b;
+    else return hook;
+  }();
+  if constexpr (SEQ) seq_hook.init();
+  if constexpr (SAMPLE) hook.a.init(a.key0, a.key1, r);
   // Workgroups of 512 or more threads run one per CU: there the bucket of
   // each lane's maximum is kept in registers rather than read back at the end.
   scan_stretch<Tin, BLOCK, U, LD, (BLOCK >= 512)>(row, a.V, vb, ve, g == 0, g == G - 1, nvec, cx, L, v, hook);
@@ -83,17 +93,35 @@ void row_features_kernel(RowArgs a) {
     return;
   }
   const uint32_t fix = rank_fixup<Tin, BLOCK>(row, a.V, nvec, cx);
+  RowCtx cf = cx;  // the context the row is finalised with
+  if constexpr (SAMPLE) {
+    // The token drawn for the row; its rank is not counted (that needs its
+    // value before the pass), and is written as 0.
+    __shared__ sample::Shared ssh;
+    __shared__ float sh_ref;
+    __shared__ uint32_t sh_def;
+    if (threadIdx.x == 0) {  // the merged state p is valid in the first wave
+      sh_ref = p.m * cx.c;
+      sh_def = (row_flags(a, r, p, cx.T) & (PR_FLAG_NONFINITE | PR_FLAG_BAD_TP)) == 0 ? 1u : 0u;
+    }
+    __syncthreads();
+    sample::pick<Tin, BLOCK, U>(row, nvec, cx, L, hook.a, sh_ref, sh_def != 0, ssh, cf.y, cf.zy);
+  }
   if constexpr (SEQ) {
     __shared__ topk::Store<BLOCK> ts;
     const topk::Lds lds = ts.view();
-    topk::select_topk<Tin, BLOCK, U>(row, a.V, cx.h, vb, ve, nvec, a.top_k, hook, lds);
+    topk::select_topk<Tin, BLOCK, U>(row, a.V, cx.h, vb, ve, nvec, a.top_k, seq_hook, lds);
     if (threadIdx.x < kWave) {  // the merged state p is valid in the first wave
       const float H = topk::topk_entropy_f32(lds.top, a.top_k, p.m, cx.c, p.S);
       const float rho = topk::position_fraction(a.offsets, a.n_req, r);
       if (threadIdx.x == 0) {
         float conf[4];
-        const uint32_t flags = finalize_row(a, r, p, cx, fix, conf);
+        const uint32_t flags = finalize_row(a, r, p, cf, fix, conf);
         write_sequence_row(a, r, conf, flags, H, rho);
+        if (SAMPLE) {
+          a.sampled_out[r] = cf.y;
+          if (a.out.rank) a.out.rank[r] = 0;
+        }
       }
     }
     return;
@@ -102,8 +130,12 @@ void row_features_kernel(RowArgs a) {
     if (!kEarlySlot) pm.fetch(a, r);
     float conf[4];
     if (threadIdx.x == 0) {
-      finalize_row(a, r, p, cx, fix, conf);
+      finalize_row(a, r, p, cf, fix, conf);
       stream_update(a.st, kEarlySlot ? ss : slot_load(a, r), conf);
+      if (SAMPLE) {
+        a.sampled_out[r] = cf.y;
+        if (a.out.rank) a.out.rank[r] = 0;
+      }
     }
     if (pm.slot >= 0) p2::feed_row(a, pm, conf);
   }
@@ -291,6 +323,31 @@ static hipError_t launch_sequence_typed(const RowArgs& a, hipStream_t stream) {
 hipError_t launch_feature_sequence(const RowArgs& a, pr_dtype dtype, hipStream_t stream) {
   if (a.n_rows == 0) return hipSuccess;
   return dtype == PR_BF16 ? launch_sequence_typed<uint16_t>(a, stream) : launch_sequence_typed<float>(a, stream);
+}
+
+// The sampling variant: the tiers of the sequence variant, with the
+// sequence X when a.X is set.
+template <typename Tin, bool SEQ>
+static hipError_t launch_sample_typed(const RowArgs& a, hipStream_t stream) {
+  constexpr int U = unroll_for<Tin>();
+  constexpr int LD = load_depth_for<Tin>();
+  constexpr int LDW = Elem<Tin>::kVec == 8 ? PR_WIDE_LOAD_DEPTH_BF16 : PR_WIDE_LOAD_DEPTH_F32;
+  const dim3 grid(static_cast<unsigned>(a.n_rows));
+  if (a.n_rows >= kWideRows) {
+    row_features_kernel<Tin, kBlock, U, LD, false, SEQ, true><<<grid, kBlock, 0, stream>>>(a);
+  } else if (a.n_rows > 256) {
+    row_features_kernel<Tin, kMidBlock, U, LDW, false, SEQ, true><<<grid, kMidBlock, 0, stream>>>(a);
+  } else {
+    row_features_kernel<Tin, kWideBlock, U, LDW, false, SEQ, true><<<grid, kWideBlock, 0, stream>>>(a);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_sample(const RowArgs& a, pr_dtype dtype, hipStream_t stream) {
+  if (a.n_rows == 0) return hipSuccess;
+  if (dtype == PR_BF16) return a.X ? launch_sample_typed<uint16_t, true>(a, stream)
+                                   : launch_sample_typed<uint16_t, false>(a, stream);
+  return a.X ? launch_sample_typed<float, true>(a, stream) : launch_sample_typed<float, false>(a, stream);
 }
 
 }  // namespace pr

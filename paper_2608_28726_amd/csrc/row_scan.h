@@ -256,7 +256,7 @@ __device__ RowCtx row_ctx(const RowArgs& a, int64_t r, const void* row) {
   cx.c = temperature_ok(T) ? kLog2e / T : kLog2e;
   cx.h = head_elems<Tin>(row, a.V);
   cx.fix_vec = 0;
-  const int32_t y = a.sampled_ids[r];
+  const int32_t y = a.sampled_ids ? a.sampled_ids[r] : -1;  // none yet when the kernel draws it
   if (y >= 0 && y < a.V) {
     cx.y = y;
     const int64_t q = static_cast<int64_t>(y) - cx.h;
