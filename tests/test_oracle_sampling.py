@@ -97,6 +97,7 @@ MUTANTS = {
 }
 
 
+@pytest.mark.filterwarnings("ignore::RuntimeWarning")  # a mutant may divide by zero
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_mutant_is_caught(name):
     old, new = MUTANTS[name]
