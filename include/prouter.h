@@ -134,7 +134,8 @@ size_t pr_token_features_workspace(pr_dtype dtype, int64_t n_rows, int32_t vocab
  *   temperature  float [n_rows], per-row temperature (finite, >= 2^-100).
  *   top_p        float [n_rows] or NULL (off). P >= 1 switches a row's
  *                truncation off; 0 < P < 1 keeps the shortest prefix of the
- *                order whose mass reaches P of the total.
+ *                order whose mass reaches P of the total. With top_p, vocab
+ *                must be below 2^24 (PR_ERR_UNSUPPORTED otherwise).
  *   out          host pointer to a struct of device output arrays, all
  *                required.
  *   workspace    device scratch of at least

@@ -21,6 +21,8 @@ struct pr_stream {
 namespace {
 
 constexpr int kStreamMaxSplit = 32;
+// The top-p histogram packs a bin's count into 24 bits.
+constexpr int32_t kTopPMaxVocab = 1 << 24;
 
 inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
@@ -116,6 +118,7 @@ pr_status pr_token_features(const void* logits, pr_dtype dtype, int64_t n_rows, 
   a.temperature = temperature;
   a.top_p = top_p;
   a.out = *out;
+  if (top_p && vocab >= kTopPMaxVocab) return PR_ERR_UNSUPPORTED;
   if (top_p) return hip_status(launch_topp(a, dtype, workspace, as_stream(stream)));
   a.G = row_split(n_rows, vocab, dtype);
   a.ws = static_cast<Partial*>(workspace);
@@ -146,6 +149,7 @@ pr_status pr_feature_sequence(const void* logits, pr_dtype dtype, int64_t n_rows
   a.offsets = offsets;
   a.n_req = n_req;
   a.top_k = top_k;
+  if (top_p && vocab >= kTopPMaxVocab) return PR_ERR_UNSUPPORTED;
   if (top_p) return hip_status(launch_topp(a, dtype, nullptr, as_stream(stream)));
   return hip_status(launch_feature_sequence(a, dtype, as_stream(stream)));
 }

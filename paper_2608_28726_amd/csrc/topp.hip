@@ -18,7 +18,7 @@
 //     margin of 5e-4. (Integer LDS atomics are far cheaper than float ones);
 //  2. an exact pass: float64 sums of mass, count and entropy term over the
 //     logits above the window, the window's logits gathered into LDS, and
-//     the float64 total over every logit within 50 nats of M;
+//     the float64 total over every binned logit;
 //  3. a bitonic sort of the window (descending) and a float64 scan along it
 //     give the exact k; the crossing is verified to lie inside the window.
 // Logits beyond 50 nats can never be in a nucleus with P < 1 (their total
@@ -58,6 +58,7 @@ constexpr float kHK = kHB / kHSpan;  // bins per nat
 constexpr int kAboveCap = 512;    // logits above the bins, kept in a list
 constexpr double kWinMargin = 5e-4;  // relative margin of the window around P * S
 constexpr float kOffQ = 4096.0f;     // fixed-point scale of the offsets from the bin centre
+constexpr int kCountShift = 40;      // a histogram word: count << kCountShift | offset sum
 
 struct TpShared {
   union {
@@ -66,8 +67,11 @@ struct TpShared {
       uint32_t cnt[kBins];
     } lg;              // fallback histogram
     struct {
-      uint32_t cnt[kHB + kWave];  // stats-pass histogram (+ one discard slot per lane)
-      int32_t off[kHB + kWave];   // summed offsets from the bin centre, times kOffQ
+      // stats-pass histogram (+ one discard slot per lane): per bin, the
+      // count (top 24 bits) and the summed offsets from the bin centre
+      // (low 40 bits: each logit adds round((offset + 1/2) * kOffQ) in
+      // [0, kOffQ], so the field stays below 2^40 while V < 2^24)
+      uint64_t bins[kHB + kWave];
     } hs;
     double wtab[kHB];  // exact pass: exp of each bin centre's distance from M
   } u;
@@ -204,14 +208,13 @@ __device__ __forceinline__ double exp_tang(double d, const double* tab) {
 
 // Stats-pass histogram: logit z counts in bin floor(bf), bf = fma(z, kz, k0)
 // = (A0 - z) / T * kHK + kHAbove * kHK, and adds its offset bf - floor(bf) -
-// 1/2 from the centre; bf < 0 (more than kHAbove nats above A0) goes to the
+// 1/2 from the centre (both in one 64-bit word); bf < 0 (more than kHAbove nats above A0) goes to the
 // list instead, bf >= kHB is beyond the window. Lanes with no bin update a
 // discard slot of their own, so the update is branch-free and discards do
 // not collide. The exact pass recomputes bf with the same operands, so both
 // passes bin identically.
 struct HistHook {
-  uint32_t* cnt;
-  int32_t* off;
+  uint64_t* bins;
   float* above;
   uint32_t* n_above;
   float kz, k0;  // bin coordinate
@@ -222,8 +225,9 @@ struct HistHook {
     const int b = static_cast<int>(bc);
     const int idx = in ? b : kHB + static_cast<int>(__lane_id());
     const float delta = bc - static_cast<float>(b) - 0.5f;  // in [-1/2, 1/2) for a counted logit
-    atomicAdd(&cnt[idx], 1u);
-    atomicAdd(&off[idx], static_cast<int32_t>(delta * kOffQ));
+    // one 64-bit atomic: count and the offset rounded to the nearest 1/kOffQ
+    const uint32_t q = static_cast<uint32_t>(fmaf(delta, kOffQ, 0.5f * kOffQ + 0.5f));
+    atomicAdd(&bins[idx], (uint64_t{1} << kCountShift) | q);
   }
   template <int N>
   __device__ __forceinline__ void step(const float (&z)[N], const float (&)[N], float cmax, int64_t, const Lane&) {
@@ -539,8 +543,10 @@ __device__ bool hist_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec
 #pragma unroll
   for (int k = 0; k < kPer; ++k) {
     const double w = exp(lead - (static_cast<double>(b0 + k) + 0.5) / kHK);
-    const double dsum = static_cast<double>(sh.u.hs.off[b0 + k]) / kOffQ;
-    wb[k] = (static_cast<double>(sh.u.hs.cnt[b0 + k]) - dsum / kHK) * w;
+    const uint64_t word = sh.u.hs.bins[b0 + k];
+    const double cnt = static_cast<double>(word >> kCountShift);
+    const double dsum = (static_cast<double>(word & ((uint64_t{1} << kCountShift) - 1)) - cnt * (0.5 * kOffQ)) / kOffQ;
+    wb[k] = (cnt - dsum / kHK) * w;
     seg += wb[k];
   }
   double tot = seg;
@@ -578,8 +584,9 @@ __device__ bool hist_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec
 #pragma unroll
   for (int k = 0; k < kPer; ++k) {
     const int b = b0 + k;
-    if (b < b_lo) above += sh.u.hs.cnt[b];
-    else if (b <= b_hi) inwin += sh.u.hs.cnt[b];
+    const uint32_t cnt = static_cast<uint32_t>(sh.u.hs.bins[b] >> kCountShift);
+    if (b < b_lo) above += cnt;
+    else if (b <= b_hi) inwin += cnt;
   }
   inwin = block_sum_u(inwin, sh) + (b_lo < 0 ? n_above : 0u);
   above = block_sum_u(above, sh) + (b_lo >= 0 ? n_above : 0u);  // counts are exact
@@ -596,13 +603,16 @@ __device__ bool hist_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec
   __syncthreads();
 
   // 2. exact pass: sums above the window, the window gathered, the total
+  // (every binned logit: those more than 50 nats below M add less than
+  // V e^-50 of S). dd = (z - M) / T by one fma: M / T is rounded once, an
+  // absolute error of about 1e-16 |M / T| in dd.
   double mA = 0.0, eA = 0.0, sT = 0.0;
-  const double M64 = static_cast<double>(D.M);
+  const double nMT = -static_cast<double>(D.M) * D.invT64;
   for_each_logit<Tin>(row, V, h, nvec, [&](float z) {
     const float bf = fmaf(z, hk.kz, hk.k0);
     if (!(bf < static_cast<float>(kHB))) return;  // beyond 50 nats below A0, -inf, NaN
     const int b = bf < 0.0f ? -1 : static_cast<int>(bf);
-    const double dd = (static_cast<double>(z) - M64) * D.invT64;
+    const double dd = fma(static_cast<double>(z), D.invT64, nMT);
     const double r = dd - fma(-static_cast<double>(b < 0 ? 0 : b), invK, c0);
     double e;
     if (b >= 0 && fabs(r) < 0.02) {
@@ -619,7 +629,7 @@ __device__ bool hist_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec
     const double fa = ab ? 1.0 : 0.0;
     mA = fma(e, fa, mA);
     eA = fma(e * dd, fa, eA);
-    sT += dd > -static_cast<double>(kDMax) ? e : 0.0;
+    sT += e;
     if (!ab && b <= b_hi) {
       const uint32_t slot = atomicAdd(&sh.wcount, 1u);
       if (slot < static_cast<uint32_t>(kCap)) sh.win[slot] = z;
@@ -653,7 +663,7 @@ __device__ bool hist_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec
   const double ce = block_exclusive_scan(se, sh);
   double wm = sm, we = se;
   block_sum2(wm, we, sh);
-  const double S = sT2;  // every logit within 50 nats of M
+  const double S = sT2;  // every binned logit
   const double target = static_cast<double>(P) * S;
   if (!(mA < target) || mA + wm < target) return false;  // crossing outside the window
   if (threadIdx.x == 0) sh.jfirst = 0xffffffffu;
@@ -736,10 +746,7 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
     for (int k = 0; k < VEC; ++k) pm = fmaxf(pm, z[k]);
   }
   pm = wave_max(pm);
-  for (int b = threadIdx.x; b < kHB + kWave; b += kTpBlock) {
-    sh.u.hs.cnt[b] = 0u;
-    sh.u.hs.off[b] = 0;
-  }
+  for (int b = threadIdx.x; b < kHB + kWave; b += kTpBlock) sh.u.hs.bins[b] = 0;
   if (threadIdx.x < 64) sh.exptab[threadIdx.x] = exp2(static_cast<double>(threadIdx.x) * (1.0 / 64.0));
   if (threadIdx.x == 0) sh.n_above = 0;
   if (threadIdx.x % kWave == 0) sh.red_f[threadIdx.x / kWave] = pm;
@@ -751,8 +758,7 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
   HookPair<HistHook, typename std::conditional<SEQ, topk::Hook, NoHook>::type> hp;
   HistHook& hk = hp.a;
   if constexpr (SEQ) hp.b.init();
-  hk.cnt = sh.u.hs.cnt;
-  hk.off = sh.u.hs.off;
+  hk.bins = sh.u.hs.bins;
   hk.above = sh.above;
   hk.n_above = &sh.n_above;
   hk.kz = anchored ? -invT * kHK : 0.0f;
