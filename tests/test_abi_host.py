@@ -110,6 +110,17 @@ def test_other_entry_points_reject_bad_arguments():
         _abi.PR_OK
 
 
+def test_topp_vocabulary_limit():
+    """The top-p histogram packs a bin's count into 24 bits."""
+    lib = ensure_built()
+    from paper_2608_28726_amd import _abi
+    p = C.c_void_p(256)
+    V = 1 << 24
+    # rejected on the host before any launch
+    assert lib.pr_feature_sequence(p, _abi.PR_F32, 4, V, V, p, p, p, p, 1, 20, p, None, None) == \
+        _abi.PR_ERR_UNSUPPORTED
+
+
 def test_calibrate_rejects_bad_arguments():
     lib = ensure_built()
     from paper_2608_28726_amd import _abi
