@@ -194,7 +194,7 @@ pr_status pr_verifier_head(const float* X, int64_t n_rows, const int32_t* offset
                            const float* weights, float* scores, void* workspace, size_t workspace_bytes,
                            void* stream) {
   if (n_rows < 0 || n_req < 0 || max_len < 1) return PR_ERR_INVALID_ARG;
-  if (n_rows > (int64_t{1} << 30)) return PR_ERR_UNSUPPORTED;
+  if (n_rows > (int64_t{1} << 30) || max_len > (1 << 20)) return PR_ERR_UNSUPPORTED;  // grid limits
   if (n_req == 0) return PR_OK;
   if (!offsets || !weights || !scores || !aligned(weights, 16)) return PR_ERR_INVALID_ARG;
   if (n_rows > 0 && (!X || !aligned(X, 4))) return PR_ERR_INVALID_ARG;

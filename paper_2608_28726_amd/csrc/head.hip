@@ -8,9 +8,9 @@
 // The tokens of all requests are processed together as rows:
 //  head_qkv_kernel   64-row tiles: (first layer: projection + encoding), the
 //                    QKV projection on MFMA (v_mfma_f32_16x16x4f32);
-//  head_attn_kernel  4 waves per (request, head, 64 queries), splitting the
-//                    request's keys: online softmax per wave, states merged
-//                    through LDS;
+//  head_attn_kernel  4 waves per (request, head, 64 queries), 16 queries
+//                    each, over all of the request's keys: scores and value
+//                    products on MFMA, online softmax per query;
 //  head_ffn_kernel   64-row tiles: output projection, residual, LayerNorm,
 //                    feed-forward (MFMA), residual, LayerNorm;
 //  head_pool_kernel  one workgroup per request: mean pool, linear, sigmoid.
@@ -206,132 +206,148 @@ __global__ __launch_bounds__(kTileThreads) void head_qkv_kernel(HeadArgs a, int 
   }
 }
 
-// Scaled dot-product attention of 64 queries (one per lane) of one request
-// and one head over all of the request's keys. The 4 waves of the workgroup
-// take turns over the key tiles of 64 (staged in each wave's own LDS, read
-// as 16-byte vectors), each keeping an online softmax in base 2 (queries
-// pre-scaled by log2(e) / sqrt(16)); the 4 partial states are then merged
-// through LDS in a fixed order.
+// Scaled dot-product attention of 64 queries of one request and one head
+// over all of the request's keys, on MFMA. Each of the 4 waves takes 16
+// queries; the workgroup stages the keys and values in tiles of 64 (double
+// buffered in LDS, rows padded to 17 floats against bank conflicts; a tile's
+// loads are issued before the current tile is computed and stored after).
+// Per group of 16 keys a wave computes the transposed scores S^T = K Q^T
+// with four v_mfma_f32_16x16x4f32 over the 16 dimensions (queries
+// pre-scaled by log2(e) / sqrt(16)), so that lane l holds the scores of
+// query l % 16 for keys 4 (l / 16) + r, r = 0..3. The 4 groups of a tile are
+// independent chains; one online-softmax update per tile and query in base
+// 2 (a query's 64 keys lie in 16 registers of 4 lanes: two cross-lane steps
+// for the maximum, two for the sum); then O += P V with 16 more, taking each
+// group's keys in the order 4m + r, in which the score registers already
+// are the matrix A operand.
 constexpr int kAttnWaves = 4;
+constexpr int kAttnQ = 16;                      // queries per wave
+constexpr int kAttnWgQ = kAttnWaves * kAttnQ;   // queries per workgroup
+constexpr int kKT = 64;                         // keys per staged tile
+constexpr int kKPad = DH + 1;                   // LDS row of one key
+typedef float fx4 __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(kAttnWaves * kWave) void head_attn_kernel(HeadArgs a) {
-  __shared__ f4 sK[kAttnWaves][kWave * DH / 4];
-  __shared__ f4 sV[kAttnWaves][kWave * DH / 4];
-  __shared__ float sM[kAttnWaves][kWave], sL[kAttnWaves][kWave];
-  __shared__ f4 sAcc[kAttnWaves][DH / 4][kWave];
+  __shared__ float sK[2][kKT * kKPad];
+  __shared__ float sV[2][kKT * kKPad];
   const int64_t req = blockIdx.x;
   const int hd = blockIdx.y;
   const int64_t lo = a.offsets[req], hi = a.offsets[req + 1];
   const int64_t T = hi - lo;
   if (T > a.max_len) return;  // scored NaN by the pool kernel
-  const int64_t q0 = lo + static_cast<int64_t>(blockIdx.z) * kWave;
+  const int64_t q0 = lo + static_cast<int64_t>(blockIdx.z) * kAttnWgQ;
   if (q0 >= hi) return;
   const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
-  const int64_t q = q0 + lane;
-  const bool valid = q < hi;
+  const int i16 = lane % 16, g = lane / 16;
+  const int64_t qw = q0 + w * kAttnQ;  // this wave's first query
   constexpr float kScale = 1.4426950408889634f / 4.0f;  // log2(e) / sqrt(DH)
-  float qv[DH];
+  // B operand of S^T: Q[qw + i16][4c + g], c = 0..3
+  float qb[4];
   {
-    const f4* qp = reinterpret_cast<const f4*>(a.qkv + (valid ? q : lo) * QKV + hd * DH);
+    const int64_t q = qw + i16;
+    const bool ok = q < hi;
+    const float* qp = a.qkv + (ok ? q : lo) * QKV + hd * DH;
 #pragma unroll
-    for (int d4 = 0; d4 < DH / 4; ++d4) {
-      const f4 t = qp[d4] * kScale;
-      qv[4 * d4] = t.x;
-      qv[4 * d4 + 1] = t.y;
-      qv[4 * d4 + 2] = t.z;
-      qv[4 * d4 + 3] = t.w;
-    }
+    for (int c = 0; c < 4; ++c) qb[c] = ok ? qp[4 * c + g] * kScale : 0.0f;
   }
-  float m = -INFINITY, l = 0.0f, acc[DH];
-#pragma unroll
-  for (int d = 0; d < DH; ++d) acc[d] = 0.0f;
-  f4* K = sK[w];
-  f4* Vt = sV[w];
-  for (int64_t k0 = lo + static_cast<int64_t>(w) * kWave; k0 < hi; k0 += kAttnWaves * kWave) {
-    const int nk = static_cast<int>(hi - k0 < kWave ? hi - k0 : kWave);
-    // wave-private tile: the wave's own LDS ops complete in order
-    if (lane < nk) {
-      const f4* src = reinterpret_cast<const f4*>(a.qkv + (k0 + lane) * QKV);
-#pragma unroll
-      for (int d4 = 0; d4 < DH / 4; ++d4) {
-        K[lane * (DH / 4) + d4] = src[(D + hd * DH) / 4 + d4];
-        Vt[lane * (DH / 4) + d4] = src[(2 * D + hd * DH) / 4 + d4];
-      }
+  // One thread per (key, 4 dimensions) of a tile.
+  const int kk = threadIdx.x / 4, d4 = threadIdx.x % 4;
+  auto load = [&](int64_t t, f4& kv, f4& vv) {
+    const int64_t key = lo + t * kKT + kk;
+    kv = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    vv = kv;
+    if (key < hi) {
+      const f4* src = reinterpret_cast<const f4*>(a.qkv + key * QKV);
+      kv = src[(D + hd * DH) / 4 + d4];
+      vv = src[(2 * D + hd * DH) / 4 + d4];
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    for (int j0 = 0; j0 < nk; j0 += 8) {
-      const int nj = nk - j0 < 8 ? nk - j0 : 8;
-      float s[8];
-      float smax = -INFINITY;
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        float t = -INFINITY;
-        if (u < nj) {
-          t = 0.0f;
-#pragma unroll
-          for (int d4 = 0; d4 < DH / 4; ++d4) {
-            const f4 k = K[(j0 + u) * (DH / 4) + d4];
-            t = fmaf(qv[4 * d4], k.x, t);
-            t = fmaf(qv[4 * d4 + 1], k.y, t);
-            t = fmaf(qv[4 * d4 + 2], k.z, t);
-            t = fmaf(qv[4 * d4 + 3], k.w, t);
-          }
-        }
-        s[u] = t;
-        smax = fmaxf(smax, t);
-      }
-      const float mn = fmaxf(m, smax);
-      const float corr = exp2f(m - mn);  // m = -inf at first: 0
-      l *= corr;
-#pragma unroll
-      for (int d = 0; d < DH; ++d) acc[d] *= corr;
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        if (u < nj) {
-          const float p = exp2f(s[u] - mn);
-          l += p;
-#pragma unroll
-          for (int d4 = 0; d4 < DH / 4; ++d4) {
-            const f4 v = Vt[(j0 + u) * (DH / 4) + d4];
-            acc[4 * d4] = fmaf(p, v.x, acc[4 * d4]);
-            acc[4 * d4 + 1] = fmaf(p, v.y, acc[4 * d4 + 1]);
-            acc[4 * d4 + 2] = fmaf(p, v.z, acc[4 * d4 + 2]);
-            acc[4 * d4 + 3] = fmaf(p, v.w, acc[4 * d4 + 3]);
-          }
-        }
-      }
-      m = mn;
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();  // the tile is read before the next one overwrites it
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-  }
-  sM[w][lane] = m;
-  sL[w][lane] = l;
-#pragma unroll
-  for (int d4 = 0; d4 < DH / 4; ++d4) sAcc[w][d4][lane] = f4{acc[4 * d4], acc[4 * d4 + 1], acc[4 * d4 + 2], acc[4 * d4 + 3]};
+  };
+  auto store = [&](int buf, const f4& kv, const f4& vv) {
+    float* kd = &sK[buf][kk * kKPad + 4 * d4];
+    float* vd = &sV[buf][kk * kKPad + 4 * d4];
+    kd[0] = kv.x;
+    kd[1] = kv.y;
+    kd[2] = kv.z;
+    kd[3] = kv.w;
+    vd[0] = vv.x;
+    vd[1] = vv.y;
+    vd[2] = vv.z;
+    vd[3] = vv.w;
+  };
+  static_assert(kAttnWaves * kWave == kKT * 4, "one thread per key and 4 dimensions");
+  float m = -INFINITY, l = 0.0f;  // of query i16 (the same in its 4 lanes)
+  fx4 acc = fx4{0.0f, 0.0f, 0.0f, 0.0f};  // O[4g + r][i16]
+  const int64_t ntiles = (T + kKT - 1) / kKT;
+  const bool busy = qw < hi;  // a wave whose queries all lie past the request only stages
+  f4 nk, nv;
+  load(0, nk, nv);
+  store(0, nk, nv);
   __syncthreads();
-  if (w == 0 && valid) {
-    float M = sM[0][lane];
+  for (int64_t t = 0; t < ntiles; ++t) {
+    const int buf = static_cast<int>(t & 1);
+    if (t + 1 < ntiles) load(t + 1, nk, nv);
+    if (busy) {
+      const float* K = sK[buf];
+      const float* Vs = sV[buf];
+      const int64_t kt0 = lo + t * kKT;
+      fx4 st[kKT / 16];
 #pragma unroll
-    for (int k = 1; k < kAttnWaves; ++k) M = fmaxf(M, sM[k][lane]);
-    float L = 0.0f;
-    f4 o[DH / 4];
+      for (int sub = 0; sub < kKT / 16; ++sub) {
+        st[sub] = fx4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-    for (int d4 = 0; d4 < DH / 4; ++d4) o[d4] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+        for (int c = 0; c < 4; ++c)
+          st[sub] = __builtin_amdgcn_mfma_f32_16x16x4f32(K[(sub * 16 + i16) * kKPad + 4 * c + g], qb[c], st[sub],
+                                                         0, 0, 0);
+      }
+      float s[kKT / 4];
+      float tm = -INFINITY;
 #pragma unroll
-    for (int k = 0; k < kAttnWaves; ++k) {
-      const float c = sM[k][lane] == -INFINITY ? 0.0f : exp2f(sM[k][lane] - M);  // a wave with no keys adds nothing
-      L = fmaf(sL[k][lane], c, L);
+      for (int sub = 0; sub < kKT / 16; ++sub) {
+        const float v[4] = {st[sub].x, st[sub].y, st[sub].z, st[sub].w};
 #pragma unroll
-      for (int d4 = 0; d4 < DH / 4; ++d4) o[d4] += sAcc[k][d4][lane] * c;
+        for (int r = 0; r < 4; ++r) {
+          const bool key_ok = kt0 + sub * 16 + 4 * g + r < hi;  // keys past the request: probability 0
+          s[4 * sub + r] = key_ok ? v[r] : -INFINITY;
+          tm = fmaxf(tm, s[4 * sub + r]);
+        }
+      }
+      tm = fmaxf(tm, __shfl_xor(tm, 16));
+      tm = fmaxf(tm, __shfl_xor(tm, 32));
+      const float mn = fmaxf(m, tm);  // finite: the tile's first key is a key of the request
+      const float corr = exp2f(m - mn);  // m = -inf at first: 0
+      float ps = 0.0f;
+#pragma unroll
+      for (int k = 0; k < kKT / 4; ++k) {
+        s[k] = exp2f(s[k] - mn);
+        ps += s[k];
+      }
+      ps += __shfl_xor(ps, 16);
+      ps += __shfl_xor(ps, 32);
+      l = fmaf(l, corr, ps);
+      m = mn;
+      // row 4g + r of O belongs to query 4g + r, whose factor lane 4g + r holds
+      acc.x *= __shfl(corr, 4 * g);
+      acc.y *= __shfl(corr, 4 * g + 1);
+      acc.z *= __shfl(corr, 4 * g + 2);
+      acc.w *= __shfl(corr, 4 * g + 3);
+#pragma unroll
+      for (int sub = 0; sub < kKT / 16; ++sub) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(s[4 * sub + r], Vs[(sub * 16 + 4 * g + r) * kKPad + i16], acc,
+                                                     0, 0, 0);
+      }
     }
-    const float inv = 1.0f / L;
-    f4* dst = reinterpret_cast<f4*>(a.att + q * D + hd * DH);
+    if (t + 1 < ntiles) store(buf ^ 1, nk, nv);
+    __syncthreads();  // tile t + 1 is staged; buffer buf is free for tile t + 2
+  }
+  if (!busy) return;
+  const float o[4] = {acc.x, acc.y, acc.z, acc.w};
 #pragma unroll
-    for (int d4 = 0; d4 < DH / 4; ++d4) dst[d4] = o[d4] * inv;
+  for (int r = 0; r < 4; ++r) {
+    const float lq = __shfl(l, 4 * g + r);
+    const int64_t q = qw + 4 * g + r;
+    if (q < hi) a.att[q * D + hd * DH + i16] = o[r] / lq;
   }
 }
 
@@ -447,7 +463,8 @@ hipError_t launch_head(const HeadArgs& args, hipStream_t stream) {
   a.qkv = H1 + a.n_rows * D;
   a.att = a.qkv + a.n_rows * QKV;
   const unsigned tiles = static_cast<unsigned>((a.n_rows + kTile - 1) / kTile);
-  const dim3 attn_grid(static_cast<unsigned>(a.n_req), NH, static_cast<unsigned>((a.max_len + kWave - 1) / kWave));
+  const dim3 attn_grid(static_cast<unsigned>(a.n_req), NH,
+                       static_cast<unsigned>((a.max_len + kAttnWgQ - 1) / kAttnWgQ));
   if (a.n_rows > 0) {
     float* Hin = H0;
     float* Hout = H1;
