@@ -485,8 +485,8 @@ def run_calibrate(args, torch, pr, wl):
 def main():
     args = parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported by this build "
-              "(rows and requests are independent: see the sharding paragraph of the design notes).",
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported. Rows and requests are "
+              "independent, so several GPUs would each take whole requests with no exchange between them.",
               file=sys.stderr)
         sys.exit(2)
     import torch
