@@ -211,3 +211,60 @@ def test_p2_stream_nonfinite_reuse_and_reset():
     for k in range(2):
         _check_slot(res, k, [_tuple(host, k)], 0.5)
     st.close()
+
+
+def test_p2_full_schedule():
+    """The 256-slot schedule at full size (V = 151,936 bf16, 1,012 steps) in
+    bounded-memory mode: every slot's count and a finite score; four
+    sampled slots' P-square quantiles equal the oracle's, fed the same
+    per-token tuples the steps returned."""
+    w = wl.WORKLOADS["stream_256slots_v151936_bf16"]
+    fin = wl.stream_schedule(w)
+    n_steps = int(fin.max())
+    rng = np.random.default_rng(21)
+    watch = [int(s) for s in rng.choice(w.n_req, 4, replace=False)]
+    tokens = {s: [] for s in watch}
+    st = pr.StreamState(w.n_req, 0, q=w.q)
+    results = {}
+    print(f"case p2 full schedule: {n_steps} steps, watching slots {watch}", flush=True)
+    for step in range(1, n_steps + 1):
+        active = np.flatnonzero(fin >= step).astype(np.int32)
+        logits, ids, T = wl.stream_step_inputs(w, step, active, device="cuda")
+        out = st.step(logits, torch.as_tensor(active).cuda(), ids, T, want_features=True)
+        rows = [int(np.searchsorted(active, s)) for s in watch if fin[s] >= step]
+        if rows:
+            sel = torch.as_tensor(rows, device="cuda")
+            host = {k: v[sel].cpu().numpy() for k, v in out.items()}
+            for j, s in enumerate([s for s in watch if fin[s] >= step]):
+                tokens[s].append(_tuple(host, j))
+        ending = active[fin[active] == step]
+        if len(ending):
+            res = st.finish(torch.as_tensor(ending).cuda(), w.tau)
+            torch.cuda.synchronize()
+            for k, s in enumerate(ending):
+                results[int(s)] = {key: v[k].cpu().numpy() for key, v in res.items()}
+    st.close()
+    assert sorted(results) == list(range(w.n_req))
+    for s in range(w.n_req):
+        assert int(results[s]["count"]) == fin[s]
+        assert np.isfinite(results[s]["score"])
+    for s in watch:
+        r = {key: np.array([v]) for key, v in results[s].items()}
+        _check_slot(r, 0, tokens[s], w.q)
+
+
+def test_calibrated_head_scores_route_the_batch():
+    """Scores from the verifier head, calibrated for a ship fraction, then
+    routed with that threshold: exactly the calibrated count ships, and tau
+    is the oracle's for the same scores."""
+    w = wl.scaled(wl.WORKLOADS["ragged_64req_v151936_bf16"], n_req=40, len_hi=24, len_lo=4, V=4096)
+    b = wl.make_batch(w, device="cuda")
+    offsets = torch.as_tensor(b.offsets).cuda()
+    X = pr.feature_sequence(b.logits, b.sampled_ids, b.temperature, offsets)
+    p = pr.verifier_head(X, offsets, torch.tensor(wl.head_weights(), device="cuda"), max_len=w.len_hi)
+    tau, ns = pr.calibrate_threshold(p, 0.6)
+    ship, n_ship = pr.route(p, float(tau.item()))
+    torch.cuda.synchronize()
+    otau, ons = oracle.calibrate_threshold(p.cpu().numpy().astype(np.float64), 0.6)
+    assert tau.item() == otau and ns.item() == ons == int(n_ship.item()) == int(ship.sum().item())
+    assert ons >= math.ceil(0.6 * w.n_req)
