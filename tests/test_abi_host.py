@@ -110,6 +110,32 @@ def test_other_entry_points_reject_bad_arguments():
         _abi.PR_OK
 
 
+def test_sample_features_rejects_bad_arguments():
+    """pr_sample_features checks everything on the host before any launch."""
+    lib = ensure_built()
+    from paper_2608_28726_amd import _abi
+    p = C.c_void_p(256)
+    bad = _abi.PR_ERR_INVALID_ARG
+    feats = _abi.TokenFeatures(*([8] * 10))
+    partial = _abi.TokenFeatures(*([8] * 9 + [0]))
+    call = lambda *a: lib.pr_sample_features(*a)
+    #          logits dtype n  V   stride T  seed off ids feats          offs n_req k   X     stream
+    assert call(p, 7, 4, 100, 100, p, 1, 0, p, C.byref(feats), None, 0, 20, None, None) == bad    # dtype
+    assert call(p, _abi.PR_F32, -1, 100, 100, p, 1, 0, p, None, None, 0, 20, None, None) == bad   # n_rows
+    assert call(p, _abi.PR_F32, 4, 1, 100, p, 1, 0, p, None, None, 0, 20, None, None) == bad      # vocab < 2
+    assert call(p, _abi.PR_F32, 4, 100, 99, p, 1, 0, p, None, None, 0, 20, None, None) == bad     # stride
+    assert call(None, _abi.PR_F32, 4, 100, 100, p, 1, 0, p, None, None, 0, 20, None, None) == bad  # logits
+    assert call(p, _abi.PR_F32, 4, 100, 100, None, 1, 0, p, None, None, 0, 20, None, None) == bad  # T
+    assert call(p, _abi.PR_F32, 4, 100, 100, p, 1, 0, None, None, None, 0, 20, None, None) == bad  # ids
+    assert call(p, _abi.PR_F32, 4, 100, 100, p, 1, 0, p, C.byref(partial), None, 0, 20, None, None) == bad
+    assert call(p, _abi.PR_F32, 4, 100, 100, p, 1, 0, p, None, None, 1, 20, p, None) == bad       # X, no offsets
+    assert call(p, _abi.PR_F32, 4, 100, 100, p, 1, 0, p, None, p, 1, 0, p, None) == bad           # top_k 0
+    assert call(p, _abi.PR_F32, 4, 100, 100, p, 1, 0, p, None, p, 1, 33, p, None) == bad          # top_k > 32
+    assert call(p, _abi.PR_F32, 4, 100, 100, p, 1, 0, p, None, p, 1, 20, C.c_void_p(260), None) == bad  # X align
+    assert call(C.c_void_p(258), _abi.PR_F32, 4, 100, 100, p, 1, 0, p, None, None, 0, 20, None, None) == bad
+    assert call(None, _abi.PR_F32, 0, 100, 100, None, 1, 0, None, None, None, 0, 20, None, None) == _abi.PR_OK
+
+
 def test_topp_vocabulary_limit():
     """The top-p histogram packs a bin's count into 24 bits."""
     lib = ensure_built()
