@@ -95,8 +95,11 @@ struct HookPair {
 // of the wave calls this together (wave-uniform control flow), so the
 // cross-lane steps below see all 64 lanes. With KEEP, keep[] receives the
 // step's vectors whenever they raise the lane's t1 (the bucket is then read
-// from registers, not memory, once the stretch is done).
-template <typename Tin, int NV, int BLOCK, bool KEEP, typename Hook = NoHook>
+// from registers, not memory, once the stretch is done). Without SOFT the
+// sums of 2^x are not formed (a caller that takes the distribution from
+// elsewhere): S0 only turns NaN on a NaN logit, so that the merged row state
+// still flags it, and the hook's exps are not computed (it gets the logits).
+template <typename Tin, int NV, int BLOCK, bool KEEP, bool SOFT = true, typename Hook = NoHook>
 __device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx& cx, Lane& L, vec4u* keep,
                                         Hook& hook) {
   constexpr int VEC = Elem<Tin>::kVec;
@@ -108,28 +111,36 @@ __device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx&
 #pragma unroll
   for (int k = 1; k < NV * VEC; ++k) cmax = fmaxf(cmax, z[k]);
 
-  // The wave shares one reference, its running maximum: every exponent
-  // argument stays <= 0 and the reference moves only on a new wave maximum.
-  if (__any(cmax > L.mw)) lane_rescale(L, wave_max(cmax), cx.c);
-
-  // Sum of 2^x and of 2^x * x. A masked logit (-inf) has x = -inf and
-  // 2^x = 0; x is clamped to a finite value so that 0 * x stays 0.
-  const float na = -L.a;
-  float ev[NV * VEC];
+  if constexpr (!SOFT) {
+    bool nan = false;
 #pragma unroll
-  for (int k = 0; k < NV * VEC; k += 2) {
-    const float x0 = fmaf(z[k], cx.c, na);
-    const float x1 = fmaf(z[k + 1], cx.c, na);
-    const float e0 = fast_exp2(x0);
-    const float e1 = fast_exp2(x1);
-    ev[k] = e0;
-    ev[k + 1] = e1;
-    L.S0 += e0;
-    L.S1 += e1;
-    L.E0 = fmaf(e0, fmaxf(x0, -kBig), L.E0);
-    L.E1 = fmaf(e1, fmaxf(x1, -kBig), L.E1);
+    for (int k = 0; k < NV * VEC; ++k) nan |= z[k] != z[k];
+    if (nan) L.S0 = __uint_as_float(0x7fc00000u);
+    hook.step(z, z, cmax, i, L);
+  } else {
+    // The wave shares one reference, its running maximum: every exponent
+    // argument stays <= 0 and the reference moves only on a new wave maximum.
+    if (__any(cmax > L.mw)) lane_rescale(L, wave_max(cmax), cx.c);
+
+    // Sum of 2^x and of 2^x * x. A masked logit (-inf) has x = -inf and
+    // 2^x = 0; x is clamped to a finite value so that 0 * x stays 0.
+    const float na = -L.a;
+    float ev[NV * VEC];
+#pragma unroll
+    for (int k = 0; k < NV * VEC; k += 2) {
+      const float x0 = fmaf(z[k], cx.c, na);
+      const float x1 = fmaf(z[k + 1], cx.c, na);
+      const float e0 = fast_exp2(x0);
+      const float e1 = fast_exp2(x1);
+      ev[k] = e0;
+      ev[k + 1] = e1;
+      L.S0 += e0;
+      L.S1 += e1;
+      L.E0 = fmaf(e0, fmaxf(x0, -kBig), L.E0);
+      L.E1 = fmaf(e1, fmaxf(x1, -kBig), L.E1);
+    }
+    hook.step(z, ev, cmax, i, L);
   }
-  hook.step(z, ev, cmax, i, L);
 
   // Rank of y: a vector wholly before y counts z >= z_y (z > next_below(z_y)),
   // any other vector counts z > z_y; ties before y inside y's own vector are
@@ -163,15 +174,20 @@ __device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx&
 }
 
 // One element outside the aligned vectors (row head or tail), per lane.
-template <typename Hook = NoHook>
+template <bool SOFT = true, typename Hook = NoHook>
 __device__ __forceinline__ void consume_scalar(float z, int64_t idx, const RowCtx& cx, Lane& L, Hook& hook) {
-  if (z > L.mw) lane_rescale(L, z, cx.c);
   if (cx.y >= 0) L.cnt += (z > cx.zy || (z == cx.zy && idx < cx.y)) ? 1u : 0u;
-  const float x = fmaf(z, cx.c, -L.a);
-  const float e = fast_exp2(x);
-  L.S0 += e;
-  L.E0 = fmaf(e, fmaxf(x, -kBig), L.E0);
-  hook.scalar(z, e, idx, L);
+  if constexpr (SOFT) {
+    if (z > L.mw) lane_rescale(L, z, cx.c);
+    const float x = fmaf(z, cx.c, -L.a);
+    const float e = fast_exp2(x);
+    L.S0 += e;
+    L.E0 = fmaf(e, fmaxf(x, -kBig), L.E0);
+    hook.scalar(z, e, idx, L);
+  } else {
+    if (z != z) L.S0 = __uint_as_float(0x7fc00000u);
+    hook.scalar(z, z, idx, L);
+  }
   // A scalar logit is a bucket of its own (t1v = -1: t1i is exact).
   if (z > L.t1) {
     L.t2 = L.t1;
@@ -387,8 +403,8 @@ __device__ __forceinline__ void stream_stretch(const vec4u* vp, int64_t vb, int6
 
 // Scan of the vector index range [vb, ve) of one row by one workgroup,
 // plus the scalar head (first) / tail (last) elements (stream_stretch does
-// the vectors; v holds the lane's first LD vectors).
-template <typename Tin, int BLOCK, int U, int LD, bool KEEP = false, typename Hook = NoHook>
+// the vectors; v holds the lane's first LD vectors). SOFT as in consume().
+template <typename Tin, int BLOCK, int U, int LD, bool KEEP = false, bool SOFT = true, typename Hook = NoHook>
 __device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve, bool do_head, bool do_tail,
                              int64_t nvec, const RowCtx& cx, Lane& L, vec4u (&v)[LD], Hook&& hook = Hook()) {
   constexpr int VEC = Elem<Tin>::kVec;
@@ -401,16 +417,18 @@ __device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve,
     for (int u = 0; u < U; ++u) keep[u] = neg_inf_vec<Tin>();
   }
   if (do_head) {
-    if (t < cx.h) consume_scalar(Elem<Tin>::load1(row, t), t, cx, L, hook);
-    const float m = wave_max(L.mw);  // one reference for the whole wave again
-    if (m > L.mw) lane_rescale(L, m, cx.c);
+    if (t < cx.h) consume_scalar<SOFT>(Elem<Tin>::load1(row, t), t, cx, L, hook);
+    if constexpr (SOFT) {
+      const float m = wave_max(L.mw);  // one reference for the whole wave again
+      if (m > L.mw) lane_rescale(L, m, cx.c);
+    }
   }
   stream_stretch<Tin, BLOCK, U, LD>(vp, vb, ve, v, [&](const vec4u* vv, int64_t j) {
-    consume<Tin, U, BLOCK, KEEP>(vv, j, cx, L, keep, hook);
+    consume<Tin, U, BLOCK, KEEP, SOFT>(vv, j, cx, L, keep, hook);
   });
   if (do_tail) {
     const int64_t tail0 = cx.h + nvec * VEC;
-    for (int64_t e = tail0 + t; e < V; e += BLOCK) consume_scalar(Elem<Tin>::load1(row, e), e, cx, L, hook);
+    for (int64_t e = tail0 + t; e < V; e += BLOCK) consume_scalar<SOFT>(Elem<Tin>::load1(row, e), e, cx, L, hook);
   }
   hook.finish(L);
   // The lanes holding the wave maximum examine the bucket where their t1 was

@@ -210,23 +210,24 @@ __device__ __forceinline__ double exp_tang(double d, const double* tab) {
 // = (A0 - z) / T * kHK + kHAbove * kHK, and adds its offset bf - floor(bf) -
 // 1/2 from the centre (both in one 64-bit word); bf < 0 (more than kHAbove nats above A0) goes to the
 // list instead, bf >= kHB is beyond the window. Lanes with no bin update a
-// discard slot of their own, so the update is branch-free and discards do
-// not collide. The exact pass recomputes bf with the same operands, so both
-// passes bin identically.
+// discard slot of their own (kHB + lane), so the update is branch-free and
+// discards do not collide. The exact pass recomputes bf with the same
+// operands, so both passes bin identically.
 struct HistHook {
   uint64_t* bins;
   float* above;
   uint32_t* n_above;
-  float kz, k0;  // bin coordinate
+  float kz, k0;     // bin coordinate
+  int32_t discard;  // this lane's discard slot
   __device__ __forceinline__ void count(float z) {
     const float bf = fmaf(z, kz, k0);
     const bool in = bf >= 0.0f && bf < static_cast<float>(kHB);
     const float bc = fminf(fmaxf(bf, 0.0f), static_cast<float>(kHB));  // NaN -> 0
     const int b = static_cast<int>(bc);
-    const int idx = in ? b : kHB + static_cast<int>(__lane_id());
-    const float delta = bc - static_cast<float>(b) - 0.5f;  // in [-1/2, 1/2) for a counted logit
-    // one 64-bit atomic: count and the offset rounded to the nearest 1/kOffQ
-    const uint32_t q = static_cast<uint32_t>(fmaf(delta, kOffQ, 0.5f * kOffQ + 0.5f));
+    const int idx = in ? b : discard;
+    // one 64-bit atomic: count and the offset from the centre rounded to the
+    // nearest 1/kOffQ, biased by 1/2: bc - floor(bc) in [0, 1) for a counted logit
+    const uint32_t q = static_cast<uint32_t>(fmaf(__builtin_amdgcn_fractf(bc), kOffQ, 0.5f));
     atomicAdd(&bins[idx], (uint64_t{1} << kCountShift) | q);
   }
   template <int N>
@@ -522,11 +523,18 @@ __device__ Nucleus legacy_nucleus(const void* row, int32_t V, int64_t h, int64_t
 // The nucleus from the stats-pass histogram and one exact pass. Returns
 // false (and leaves nuc unset) when the row must take the three-pass method.
 template <typename Tin>
-__device__ bool hist_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec, const Dist& D, float P,
+__device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec, const Dist& D, float P,
                              float A0, const HistHook& hk, TpShared& sh, Nucleus& nuc) {
   const double* tab = sh.exptab;
   const uint32_t n_above = sh.n_above;
   if (n_above > static_cast<uint32_t>(kAboveCap)) return false;
+  // The float32 bin coordinate bf is within a fraction of a bin of the exact
+  // one while |k0| < 2^18 (kz and k0 carry a relative error below 2.4e-7,
+  // and a binned logit has |z kz| < |k0| + kHB): every binned logit then
+  // lies within 0.012 nats of its bin centre, where the exact pass's
+  // degree-5 polynomial is accurate to 3e-15. Rows with larger |A0| / T
+  // (beyond about 4,800) take the three-pass method.
+  if (!(fabsf(hk.k0) < 0x1p18f)) return false;
 
   // 1. the window of bins around P * (total): a logit of bin b lies at
   // (b + 1/2 + delta) / kHK - kHAbove nats below A0; with w = 1/kHK the bin's
@@ -593,9 +601,8 @@ __device__ bool hist_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec
   if (inwin > static_cast<uint32_t>(kCap)) return false;
   // The counts are consumed: the same LDS now holds exp(centre of bin b - M).
   // A logit of bin b is exp(dd) = wtab[b] * exp(dd - centre), and |dd - centre|
-  // is at most half a bin (0.0092 nats) plus the float32 rounding of bf:
-  // degree-5 Taylor polynomial (truncation below 1e-14 while |dd - centre| <
-  // 0.02; otherwise, and for the list, the table-driven exp).
+  // is at most half a bin (0.0092 nats) plus the float32 rounding of bf (see
+  // above): degree-5 Taylor polynomial; the list takes the table-driven exp.
   const double invK = 1.0 / static_cast<double>(kHK);
   const double c0 = lead - 0.5 * invK;  // centre of bin b: c0 - b * invK
 #pragma unroll
@@ -604,38 +611,44 @@ __device__ bool hist_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec
 
   // 2. exact pass: sums above the window, the window gathered, the total
   // (every binned logit: those more than 50 nats below M add less than
-  // V e^-50 of S). dd = (z - M) / T by one fma: M / T is rounded once, an
-  // absolute error of about 1e-16 |M / T| in dd.
-  double mA = 0.0, eA = 0.0, sT = 0.0;
-  const double nMT = -static_cast<double>(D.M) * D.invT64;
+  // V e^-50 of S). With u = (z - M) / T - c0 by one fma (the row constant
+  // -M / T - c0 is rounded once: a common factor of every mass, which the
+  // cutoff test does not see), a logit of bin b sits r = u + b / kHK from
+  // its bin centre and dd = u + c0 nats below M; the entropy sum above the
+  // window is taken as sum e u + c0 * sum e.
+  double mA = 0.0, eAu = 0.0, sT = 0.0;
+  const double nMTc = -static_cast<double>(D.M) * D.invT64 - c0;
   for_each_logit<Tin>(row, V, h, nvec, [&](float z) {
     const float bf = fmaf(z, hk.kz, hk.k0);
     if (!(bf < static_cast<float>(kHB))) return;  // beyond 50 nats below A0, -inf, NaN
-    const int b = bf < 0.0f ? -1 : static_cast<int>(bf);
-    const double dd = fma(static_cast<double>(z), D.invT64, nMT);
-    const double r = dd - fma(-static_cast<double>(b < 0 ? 0 : b), invK, c0);
+    const double u = fma(static_cast<double>(z), D.invT64, nMTc);
+    int b;
     double e;
-    if (b >= 0 && fabs(r) < 0.02) {
+    if (bf >= 0.0f) {
+      b = static_cast<int>(bf);
+      const double r = fma(static_cast<double>(b), invK, u);
       double q = fma(r, 1.0 / 120.0, 1.0 / 24.0);
       q = fma(q, r, 1.0 / 6.0);
       q = fma(q, r, 0.5);
       q = fma(q, r, 1.0);
       q = fma(q, r, 1.0);
       e = sh.u.wtab[b] * q;
-    } else {  // the list above the bins, or a bin far off through float32 rounding of bf (huge logits)
-      e = exp_tang(fmax(dd, -700.0), tab);
+    } else {  // the list above the bins
+      b = -1;
+      e = exp_tang(fmax(u + c0, -700.0), tab);
     }
     const bool ab = b < b_lo;
     const double fa = ab ? 1.0 : 0.0;
     mA = fma(e, fa, mA);
-    eA = fma(e * dd, fa, eA);
+    eAu = fma(e * u, fa, eAu);
     sT += e;
     if (!ab && b <= b_hi) {
       const uint32_t slot = atomicAdd(&sh.wcount, 1u);
       if (slot < static_cast<uint32_t>(kCap)) sh.win[slot] = z;
     }
   });
-  block_sum2(mA, eA, sh);
+  block_sum2(mA, eAu, sh);
+  const double eA = fma(c0, mA, eAu);
   double sT2 = sT, unused = 0.0;
   block_sum2(sT2, unused, sh);
   const uint32_t cA = above;
@@ -699,6 +712,29 @@ __device__ bool hist_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec
 
 }  // namespace
 
+// The first pass of a row without a nucleus (P >= 1, or a rejected P or
+// temperature): the plain scan with its sums of 2^x, and the top-K hook
+// (no histogram). Kept out of line, so that the kernel body around the
+// nucleus path stays compact; its state goes in and comes back by value, so
+// that no address of the kernel's scan state (lane, prefetched vectors,
+// histogram hook) escapes into a call, which would move that state into
+// private memory for the nucleus path too.
+template <int LD>
+struct Prefetched {
+  vec4u v[LD];
+};
+template <typename HookB>
+struct PlainResult {
+  Lane L;
+  HookB hb;
+};
+template <typename Tin, int LD, typename HookB>
+__device__ __noinline__ PlainResult<HookB> plain_pass(const void* row, int32_t V, int64_t nvec, RowCtx cx, Lane L,
+                                                      Prefetched<LD> pre, HookB hb) {
+  scan_stretch<Tin, kTpBlock, 2, LD, false, true>(row, V, 0, nvec, true, true, nvec, cx, L, pre.v, hb);
+  return PlainResult<HookB>{L, hb};
+}
+
 // LDS of the top-K selection, inside the window buffer (unused until the
 // nucleus is computed) except for the result.
 __device__ __forceinline__ topk::Lds topk_lds(TpShared& sh) {
@@ -753,7 +789,12 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
   __syncthreads();
   float A0 = sh.red_f[0];
   for (int k = 1; k < kNW; ++k) A0 = fmaxf(A0, sh.red_f[k]);
-  const bool anchored = A0 > -INFINITY && A0 < INFINITY && temperature_ok(cx.T);
+  // A row whose nucleus is computed (0 < P < 1, valid temperature) takes its
+  // distribution from the float64 sums of the nucleus, so its first pass
+  // forms no exps; any other row gets the plain features and no histogram.
+  const float Prow = a.top_p[r];
+  const bool nucleus_row = Prow > 0.0f && Prow < 1.0f && temperature_ok(cx.T);
+  const bool anchored = nucleus_row && A0 > -INFINITY && A0 < INFINITY;
   const float invT = 1.0f / cx.T;
   HookPair<HistHook, typename std::conditional<SEQ, topk::Hook, NoHook>::type> hp;
   HistHook& hk = hp.a;
@@ -761,13 +802,25 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
   hk.bins = sh.u.hs.bins;
   hk.above = sh.above;
   hk.n_above = &sh.n_above;
+  hk.discard = kHB + static_cast<int32_t>(threadIdx.x % kWave);
   hk.kz = anchored ? -invT * kHK : 0.0f;
   hk.k0 = anchored ? fmaf(A0, invT * kHK, kHAbove * kHK) : INFINITY;  // unanchored: nothing binned
 
-  // 1. stats pass, building the histogram
+  // 1. stats pass, building the histogram (S and E of the merged state are
+  // only formed for a row without a nucleus)
   Lane L;
   lane_init(L);
-  scan_stretch<Tin, kTpBlock, 2, kLD, false>(row, a.V, 0, nvec, true, true, nvec, cx, L, v, hp);
+  if (nucleus_row) {
+    [[clang::always_inline]] scan_stretch<Tin, kTpBlock, 2, kLD, false, false>(row, a.V, 0, nvec, true, true, nvec,
+                                                                               cx, L, v, hp);
+  } else {
+    Prefetched<kLD> pre;
+#pragma unroll
+    for (int u = 0; u < kLD; ++u) pre.v[u] = v[u];
+    const auto res = plain_pass<Tin>(row, a.V, nvec, cx, L, pre, hp.b);
+    L = res.L;
+    hp.b = res.hb;
+  }
   Partial p = block_merge<kTpBlock>(L, cx.c);
   const uint32_t fix = rank_fixup<Tin, kTpBlock>(row, a.V, nvec, cx);
   if constexpr (SEQ) {
@@ -777,8 +830,7 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
   if (threadIdx.x == 0) {
     sh.p = p;
     sh.fix = fix;
-    const float P = a.top_p[r];
-    sh.active = (row_flags(a, r, p, cx.T) & (PR_FLAG_NONFINITE | PR_FLAG_BAD_TP)) == 0 && P < 1.0f;
+    sh.active = nucleus_row && (row_flags(a, r, p, cx.T) & (PR_FLAG_NONFINITE | PR_FLAG_BAD_TP)) == 0;
   }
   __syncthreads();
   p = sh.p;
@@ -807,7 +859,7 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
   D.M = p.m;
   D.invT = 1.0f / T;
   D.invT64 = 1.0 / static_cast<double>(T);
-  const float P = a.top_p[r];
+  const float P = Prow;
   Nucleus nuc;
   if (!(anchored && hist_nucleus<Tin>(row, a.V, cx.h, nvec, D, P, A0, hk, sh, nuc)))
     nuc = legacy_nucleus<Tin>(row, a.V, cx.h, nvec, D, P, sh);

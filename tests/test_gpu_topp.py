@@ -97,7 +97,8 @@ def test_topp_histogram_edge_rows(dtype):
     """Rows aimed at each branch of the two-read method: no finite anchor
     (the first vectors all -inf), more logits far above the anchor than the
     list holds, a crossing inside that list (one dominant spike), a nucleus
-    spanning the list and the bins, and a near-flat row with a wide window."""
+    spanning the list and the bins, a near-flat row with a wide window, and
+    large logits on both sides of the limit on |A0| / T of the binning."""
     V = 65536
     rng = np.random.default_rng(77)
     rows, ids, Ts, Ps = [], [], [], []
@@ -112,6 +113,8 @@ def test_topp_histogram_edge_rows(dtype):
     z = rng.normal(0, 1, V); z[60000] = 42.0
     add(z, 123, 4.0, 0.95)                                   # spike 10 nats above the bulk at T = 4
     add(rng.normal(0, 0.01, V), 5, 1.2, 0.93)                # near-flat: wide window
+    add(rng.normal(0, 1.5, V) + 3000.0, 77, 1.0, 0.9)        # |A0| / T near 3,000: exact pass, coarse bf
+    add(rng.normal(0, 1.5, V) + 30000.0, 78, 1.0, 0.9)       # |A0| / T beyond the binning guard: three passes
     logits, ids, T, P = _run(np.stack(rows), ids, Ts, Ps, dtype)
     print(f"case topp histogram edges {dtype}", flush=True)
     compare_features(gpu_features(logits, ids, T, P), oracle_features(logits, ids, T, P))
