@@ -600,9 +600,12 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   above = block_sum_u(above, sh) + (b_lo >= 0 ? n_above : 0u);  // counts are exact
   if (inwin > static_cast<uint32_t>(kCap)) return false;
   // The counts are consumed: the same LDS now holds exp(centre of bin b - M).
-  // A logit of bin b is exp(dd) = wtab[b] * exp(dd - centre), and |dd - centre|
-  // is at most half a bin (0.0092 nats) plus the float32 rounding of bf (see
-  // above): degree-5 Taylor polynomial; the list takes the table-driven exp.
+  // A logit of bin b is exp(dd) = wtab[b] * exp(r), r = dd - centre, |r| at
+  // most half a bin (0.0092 nats) plus the float32 rounding of bf (see
+  // above): the degree-5 Taylor polynomial 1 + r + r^2 / 2 + r^3 c(r), c(r)
+  // = 1/6 + r/24 + r^2/120 taken in float32 (its rounding, below 1.5e-8,
+  // moves the polynomial by less than |r|^3 1.5e-8 < 2.5e-14). The list
+  // takes the table-driven exp.
   const double invK = 1.0 / static_cast<double>(kHK);
   const double c0 = lead - 0.5 * invK;  // centre of bin b: c0 - b * invK
 #pragma unroll
@@ -627,9 +630,9 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
     if (bf >= 0.0f) {
       b = static_cast<int>(bf);
       const double r = fma(static_cast<double>(b), invK, u);
-      double q = fma(r, 1.0 / 120.0, 1.0 / 24.0);
-      q = fma(q, r, 1.0 / 6.0);
-      q = fma(q, r, 0.5);
+      const float rf = static_cast<float>(r);
+      const float cf = fmaf(rf, fmaf(rf, 1.0f / 120.0f, 1.0f / 24.0f), 1.0f / 6.0f);
+      double q = fma(static_cast<double>(cf), r, 0.5);
       q = fma(q, r, 1.0);
       q = fma(q, r, 1.0);
       e = sh.u.wtab[b] * q;
@@ -638,9 +641,9 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
       e = exp_tang(fmax(u + c0, -700.0), tab);
     }
     const bool ab = b < b_lo;
-    const double fa = ab ? 1.0 : 0.0;
-    mA = fma(e, fa, mA);
-    eAu = fma(e * u, fa, eAu);
+    const double ea = ab ? e : 0.0;
+    mA += ea;
+    eAu = fma(ea, u, eAu);
     sT += e;
     if (!ab && b <= b_hi) {
       const uint32_t slot = atomicAdd(&sh.wcount, 1u);
