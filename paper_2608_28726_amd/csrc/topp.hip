@@ -640,12 +640,11 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
       b = -1;
       e = exp_tang(fmax(u + c0, -700.0), tab);
     }
-    const bool ab = b < b_lo;
-    const double ea = ab ? e : 0.0;
-    mA += ea;
-    eAu = fma(ea, u, eAu);
     sT += e;
-    if (!ab && b <= b_hi) {
+    if (b < b_lo) {  // above the window (lanes outside it keep their sums as they are)
+      mA += e;
+      eAu = fma(e, u, eAu);
+    } else if (b <= b_hi) {
       const uint32_t slot = atomicAdd(&sh.wcount, 1u);
       if (slot < static_cast<uint32_t>(kCap)) sh.win[slot] = z;
     }
