@@ -225,6 +225,12 @@ __device__ __forceinline__ void rebase(bool no_finite, float a_l, float A, float
   S = s * S;
 }
 
+// ln S of a row's sum of exps relative to its largest logit (S >= 1: that
+// logit contributes 1). Below 2, S - 1 is exact (Sterbenz) and log1p keeps
+// the relative precision of the small logarithm of an almost one-hot row.
+__device__ __forceinline__ float ln_sum(float S) { return S < 2.0f ? log1pf(S - 1.0f) : logf(S); }
+__device__ __forceinline__ double ln_sum(double S) { return S < 2.0 ? log1p(S - 1.0) : log(S); }
+
 // Smallest accepted temperature: keeps log2(e) / T finite in float32.
 constexpr float kMinTemperature = 0x1p-100f;
 

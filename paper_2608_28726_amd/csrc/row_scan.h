@@ -526,7 +526,7 @@ __device__ uint32_t finalize_row(const RowArgs& a, int64_t r, const Partial& p, 
     argmax = p.t1i;
     if (cx.y >= 0) rank = static_cast<int32_t>(1u + p.cnt + fix);
     if (nuc) {
-      const double lnS = log(nuc->S);
+      const double lnS = ln_sum(nuc->S);
       lse = static_cast<float>(static_cast<double>(p.m) / static_cast<double>(T) + lnS);
       entropy = static_cast<float>(lnS - nuc->E / nuc->S);
       maxprob = static_cast<float>(1.0 / nuc->S);
@@ -549,7 +549,7 @@ __device__ uint32_t finalize_row(const RowArgs& a, int64_t r, const Partial& p, 
       const float sc = fast_exp2(-delta);
       const float S = p.S * sc;
       const float E = sc * fmaf(-delta, p.S, p.E);
-      const float lnS = logf(S);
+      const float lnS = ln_sum(S);
       lse = max_logit + lnS;
       entropy = lnS - kLn2 * (E / S);
       maxprob = 1.0f / S;

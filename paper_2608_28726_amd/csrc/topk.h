@@ -421,7 +421,7 @@ __device__ __forceinline__ float topk_entropy_f32(const float* top, int j, float
   const float A = M * c;
   const float delta = fmaf(M, c, -A);
   const float S = S_raw * fast_exp2(-delta);
-  const float lnS = logf(S);
+  const float lnS = ln_sum(S);
   float term = 0.0f;
   const int l = __lane_id();
   if (l < j) {
@@ -437,7 +437,7 @@ __device__ __forceinline__ float topk_entropy_f32(const float* top, int j, float
 
 // The same over a nucleus: p = exp((z - M) / T) / S_N in float64.
 __device__ __forceinline__ float topk_entropy_f64(const float* top, int j, float M, float T, double S_N) {
-  const double lnS = log(S_N);
+  const double lnS = ln_sum(S_N);
   double term = 0.0;
   const int l = __lane_id();
   if (l < j) {
