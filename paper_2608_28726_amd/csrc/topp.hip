@@ -542,21 +542,26 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   // sum delta) (second-order error below count * w^2 / 8). Masses relative
   // to M.
   const double lead = (static_cast<double>(A0) - static_cast<double>(D.M)) * D.invT64 + kHAbove;
+  const double invK = 1.0 / static_cast<double>(kHK);
+  // Kept compact (it runs once per row): the loops over a thread's kPer bins
+  // are not unrolled (one copy of the float64 exp each; the second loop
+  // recomputes the masses of the first), and the crossing bins are found
+  // with a ballot and one LDS atomic per wave.
+  auto bin_mass = [&](int b) -> double {
+    const double w = exp(fma(-(static_cast<double>(b) + 0.5), invK, lead));
+    const uint64_t word = sh.u.hs.bins[b];
+    const double cnt = static_cast<double>(static_cast<uint32_t>(word >> kCountShift));
+    const double dsum =
+        (static_cast<double>(word & ((uint64_t{1} << kCountShift) - 1)) - cnt * (0.5 * kOffQ)) * (1.0 / kOffQ);
+    return fma(-dsum, invK, cnt) * w;
+  };
   double sa = 0.0;
   for (uint32_t i = threadIdx.x; i < n_above; i += kTpBlock) sa += exp_tang(D.d64(sh.above[i]), tab);
   constexpr int kPer = kHB / kTpBlock;
   const int b0 = threadIdx.x * kPer;
-  double wb[kPer];
   double seg = 0.0;
-#pragma unroll
-  for (int k = 0; k < kPer; ++k) {
-    const double w = exp(lead - (static_cast<double>(b0 + k) + 0.5) / kHK);
-    const uint64_t word = sh.u.hs.bins[b0 + k];
-    const double cnt = static_cast<double>(word >> kCountShift);
-    const double dsum = (static_cast<double>(word & ((uint64_t{1} << kCountShift) - 1)) - cnt * (0.5 * kOffQ)) / kOffQ;
-    wb[k] = (cnt - dsum / kHK) * w;
-    seg += wb[k];
-  }
+#pragma unroll 1
+  for (int k = 0; k < kPer; ++k) seg += bin_mass(b0 + k);
   double tot = seg;
   block_sum2(sa, tot, sh);
   tot += sa;
@@ -569,19 +574,24 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   }
   __syncthreads();
   {
+    // this thread's first bins where the running mass reaches t_lo and t_hi
+    int k_lo = kHB, k_hi = kHB;
     double c = before;
-    bool lo_done = false, hi_done = false;
-#pragma unroll
+#pragma unroll 1
     for (int k = 0; k < kPer; ++k) {
-      c += wb[k];
-      if (!lo_done && c >= t_lo) {
-        atomicMin(&sh.hb_lo, b0 + k);
-        lo_done = true;
-      }
-      if (!hi_done && c >= t_hi) {
-        atomicMin(&sh.hb_hi, b0 + k);
-        hi_done = true;
-      }
+      c += bin_mass(b0 + k);
+      if (k_lo == kHB && c >= t_lo) k_lo = b0 + k;
+      if (k_hi == kHB && c >= t_hi) k_hi = b0 + k;
+    }
+    // bins grow with the thread index: a wave's smallest candidate is that
+    // of its first lane that has one
+    const uint64_t m_lo = __ballot(k_lo < kHB);
+    const uint64_t m_hi = __ballot(k_hi < kHB);
+    const int f_lo = __shfl(k_lo, m_lo ? static_cast<int>(__builtin_ctzll(m_lo)) : 0);
+    const int f_hi = __shfl(k_hi, m_hi ? static_cast<int>(__builtin_ctzll(m_hi)) : 0);
+    if (threadIdx.x % kWave == 0) {
+      if (m_lo) atomicMin(&sh.hb_lo, f_lo);
+      if (m_hi) atomicMin(&sh.hb_hi, f_hi);
     }
   }
   if (threadIdx.x == 0) sh.wcount = 0;
@@ -589,7 +599,7 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   const int b_lo = sa >= t_lo ? -1 : sh.hb_lo;  // -1: the list above the bins
   const int b_hi = sa >= t_hi ? -1 : sh.hb_hi;
   uint32_t inwin = 0, above = 0;
-#pragma unroll
+#pragma unroll 1
   for (int k = 0; k < kPer; ++k) {
     const int b = b0 + k;
     const uint32_t cnt = static_cast<uint32_t>(sh.u.hs.bins[b] >> kCountShift);
@@ -606,9 +616,8 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   // = 1/6 + r/24 + r^2/120 taken in float32 (its rounding, below 1.5e-8,
   // moves the polynomial by less than |r|^3 1.5e-8 < 2.5e-14). The list
   // takes the table-driven exp.
-  const double invK = 1.0 / static_cast<double>(kHK);
   const double c0 = lead - 0.5 * invK;  // centre of bin b: c0 - b * invK
-#pragma unroll
+#pragma unroll 1
   for (int k = 0; k < kPer; ++k) sh.u.wtab[b0 + k] = exp(fma(-static_cast<double>(b0 + k), invK, c0));
   __syncthreads();
 
