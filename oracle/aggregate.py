@@ -10,7 +10,7 @@ p >= tau (Sec. 3.1, the paragraph defining the gain, Eq. 1). The ablation
 (Sec. 4.2, Table "ablation", row "quantile summary + MLP") shows that a
 quantile summary of the sequence is a working verifier input.
 
-Readings where the paper is silent (each is listed in the design doc):
+Readings where the paper is silent:
 
 R8   The summarised features are the confidence-oriented tuple
      A = (logprob, maxprob, -entropy, margin): the paper negates the entropy

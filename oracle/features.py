@@ -12,7 +12,7 @@ to the feature set max logit, logsumexp, softmax entropy, sampled-token
 log-probability, top-1/top-2 margin and sampled-token rank, all taken after
 temperature and optional top-p (nucleus) truncation.
 
-Readings where the paper is silent (each is listed in the design doc):
+Readings where the paper is silent:
 
 R1  Logits arrive as IEEE float32 or bfloat16 bit patterns; they are decoded
     exactly to float64. NaN or +inf anywhere, or a row that is all -inf, is

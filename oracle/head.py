@@ -11,7 +11,7 @@ outputs the request's shipping confidence p; the request ships iff p >= tau
 (Sec. 3.1, with the gain, Eq. 1). Sec. 4.2 (the signal-latency paragraph and
 Table "ablation") gives two encoder layers and about 67k parameters.
 
-Readings where the paper is silent (each is listed in the design doc):
+Readings where the paper is silent:
 
 R17  Width d = 64 and feed-forward width 128: with biases and two LayerNorms
      per layer this is 67,329 parameters, the paper's "about 67k". The

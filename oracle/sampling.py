@@ -12,7 +12,7 @@ the probability of every token, against which the draws are tested, and
 the features of a drawn row are those of :func:`oracle.token_features` for
 the drawn id.
 
-Reading (listed in DESIGN.md):
+Reading:
 
 R23  Token v is drawn with probability p_v = e_v / S, e_v = exp((z_v - M)/T),
      S = sum of e_v, over the decoded logits (R1, R3), without top-p.

@@ -11,7 +11,7 @@ H_t = -sum over the K most probable tokens of p_t(v) log p_t(v) (K = 20), and
 the position fraction rho_t = t / T. Stacked over the request's T tokens they
 form the verifier's input X (T rows, 4 columns).
 
-Readings where the paper is silent (each is listed in the design doc):
+Readings where the paper is silent:
 
 R14  p_t is the decoding distribution after temperature and top-p, the same
      distribution that l_t and m_t are taken on (see features.py, R3 and R4).

@@ -614,7 +614,7 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   // most half a bin (0.0092 nats) plus the float32 rounding of bf (see
   // above): the degree-5 Taylor polynomial 1 + r + r^2 / 2 + r^3 c(r), c(r)
   // = 1/6 + r/24 + r^2/120 taken in float32 (its rounding, below 1.5e-8,
-  // moves the polynomial by less than |r|^3 1.5e-8 < 2.5e-14). The list
+  // moves the polynomial by less than |r|^3 1.5e-8 < 3e-14). The list
   // takes the table-driven exp.
   const double c0 = lead - 0.5 * invK;  // centre of bin b: c0 - b * invK
 #pragma unroll 1
