@@ -61,6 +61,30 @@ def test_topp_special_rows():
     compare_features(gpu_features(logits, ids, T, P), oracle_features(logits, ids, T, P))
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_topp_undefined_rows_with_a_nucleus(dtype):
+    """Rows with 0 < P < 1 whose distribution is undefined: their first pass
+    forms no exps, so a NaN must still mark the row (in the vector body and
+    in the scalar tail, V = 67); +inf and all -inf rows; a rejected
+    temperature (the plain pass); one ordinary row as a control."""
+    V = 67
+    rng = np.random.default_rng(67)
+    base = rng.normal(0, 1, (6, V))
+    base[0, 10] = np.nan                     # NaN among the vectors
+    base[1, 66] = np.nan                     # NaN in the tail
+    base[2, 5] = np.inf                      # +inf
+    base[3] = -np.inf                        # every token masked
+    T = [1.0, 1.0, 1.0, 1.0, 0.0, 0.8]       # row 4: rejected temperature
+    P = [0.9, 0.9, 0.9, 0.9, 0.9, 0.9]
+    ids = [3, 4, 5, 6, 7, 8]
+    logits, ids, T, P = _run(base, ids, T, P, dtype)
+    print(f"case topp undefined rows {dtype}", flush=True)
+    g = gpu_features(logits, ids, T, P)
+    assert (g["flags"][:4] & pr.FLAG_NONFINITE).all() and g["flags"][4] & pr.FLAG_BAD_TP
+    assert g["flags"][5] & (pr.FLAG_NONFINITE | pr.FLAG_BAD_TP) == 0
+    compare_features(g, oracle_features(logits, ids, T, P))
+
+
 @pytest.mark.parametrize("V", [262144, 151936])
 def test_topp_massive_ties_radix_path(V):
     """Rows whose boundary bins hold more logits than the LDS sort takes:
@@ -130,6 +154,18 @@ def test_topp_workload_scaled():
     o = oracle_features(logits, ids, T, P)
     compare_features(g, o)
     assert (o["flags"] & pr.FLAG_OUTSIDE_NUCLEUS == 0).all()  # the sampler stays inside the nucleus
+
+
+def test_topp_bf16_large_vocabulary():
+    """The top-p row model on bf16 rows of the MLLM vocabulary (V = 151,936):
+    the bf16 instantiation of the two-read method on realistic rows, every
+    row against the oracle."""
+    w = wl.scaled(wl.WORKLOADS["topp_128x256_v262144_f32"], n_req=6, len_hi=8, V=151936, dtype="bf16")
+    b = wl.make_batch(w, device="cpu")
+    logits, ids, T, P = to_dev(b.logits, b.sampled_ids, b.temperature, b.top_p)
+    assert logits.dtype == torch.bfloat16
+    print(f"case topp bf16 V=151936 rows={b.n_rows}", flush=True)
+    compare_features(gpu_features(logits, ids, T, P), oracle_features(logits, ids, T, P))
 
 
 def test_topp_full_size():
