@@ -221,6 +221,33 @@ def test_topp_small_nuclei_bf16_f32(dtype):
     compare_sequence(Xg, Xo, amb)
 
 
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_topp_undefined_rows(dtype):
+    """The sequence variant on rows with 0 < P < 1 whose distribution is
+    undefined (a NaN among the vectors and in the scalar tail, +inf, all
+    -inf, a rejected temperature): l, m and h are NaN, rho is not; the
+    ordinary rows around them match the oracle."""
+    rng = np.random.default_rng(13)
+    n, V = 8, 1027
+    z = rng.normal(0, 2, (n, V))
+    z[0, 100] = np.nan
+    z[1, 1026] = np.nan
+    z[2, 7] = np.inf
+    z[3] = -np.inf
+    T = np.full(n, 0.9)
+    T[4] = 0.0
+    P = np.full(n, 0.85)
+    ids = rng.integers(0, V, n)
+    logits, ids, T, P = to_dev(torch.tensor(z, dtype=torch.float32).to(dtype), torch.tensor(ids, dtype=torch.int32),
+                               torch.tensor(T, dtype=torch.float32), torch.tensor(P, dtype=torch.float32))
+    off = np.array([0, 3, 6, n], dtype=np.int32)
+    print(f"case seq topp undefined rows {dtype}", flush=True)
+    Xg = gpu_sequence(logits, ids, T, off, P=P, K=20)
+    assert np.isnan(Xg[:5, :3]).all() and np.isfinite(Xg[:, 3]).all()
+    Xo, amb = oracle_sequence(logits, ids, T, off, P=P, K=20)
+    compare_sequence(Xg, Xo, amb)
+
+
 @pytest.mark.parametrize("topp", [False, True])
 def test_features_from_the_same_pass(topp):
     """features=True gives the per-token features in the same pass: parity
