@@ -508,14 +508,7 @@ def main():
     achieved = bytes_launch / (avg_ms * 1e-3) / 1e9
     log(f"[bench] {ms_per_step:.3f} ms/step, row kernel {avg_ms:.3f} ms ({achieved:.0f} GB/s)")
 
-    traffic = None
-    if os.path.exists(args.traffic_json):
-        try:
-            t = json.load(open(args.traffic_json)).get(traffic_key(w.name, args.path))
-            if t and t.get("kernel_source_hash") == kernel_source_hash(t.get("kernel", "")):
-                traffic = t["bytes_per_launch"]
-        except (OSError, ValueError, KeyError):
-            traffic = None
+    traffic = stored_traffic(args.traffic_json, w.name, args.path)
 
     result = {
         "metric": "verified token rows/sec and achieved HBM GB/s (% of peak), V=151,936 bf16",
@@ -576,6 +569,20 @@ KERNEL_SOURCES = {
 def traffic_key(workload: str, path: str) -> str:
     """Key of a workload's stored counter traffic (one entry per measured path)."""
     return workload if path == "features" else f"{workload}:{path}"
+
+
+def stored_traffic(traffic_json: str, workload: str, path: str):
+    """HBM bytes per launch from the stored counter runs of this workload and
+    path, or None: no record, or one taken on other kernel sources."""
+    if not os.path.exists(traffic_json):
+        return None
+    try:
+        t = json.load(open(traffic_json)).get(traffic_key(workload, path))
+        if t and t.get("kernel_source_hash") == kernel_source_hash(t.get("kernel", "")):
+            return t["bytes_per_launch"]
+    except (OSError, ValueError, KeyError):
+        pass
+    return None
 
 
 def kernel_source_hash(kernel: str) -> str:
