@@ -64,6 +64,31 @@ def _check_rows(logits, sampled_ids, temperature, top_p):
             raise ValueError(f"{name} must be a contiguous 1-D {dt} CUDA tensor of length {n}")
 
 
+def _check_features(f: dict, device, n: int | None, what: str, fields=_abi.FEATURE_FIELDS):
+    """Caller-supplied per-token feature tensors: each of `fields` present,
+    1-D, contiguous, on `device`, of its dtype, and n long when n is given
+    (a tensor on the host would reach a kernel as a host pointer)."""
+    for k in fields:
+        t = f.get(k)
+        dt = torch.float32 if k in FEATURE_FLOATS else torch.int32
+        if (t is None or t.dtype != dt or t.device != device or t.dim() != 1 or not t.is_contiguous()
+                or (n is not None and t.shape[0] != n)):
+            size = "" if n is None else f" of length {n}"
+            raise ValueError(f"{what}['{k}'] must be a contiguous 1-D {dt} tensor{size} on {device}")
+
+
+def _check_workspace(workspace, device):
+    if workspace is not None and (workspace.device != device or not workspace.is_contiguous()):
+        raise ValueError(f"workspace must be a contiguous tensor on {device}")
+
+
+def _check_index_tensor(t, name: str, device, n: int | None = None):
+    if (t.dtype != torch.int32 or t.device != device or t.dim() != 1 or not t.is_contiguous()
+            or (n is not None and t.shape[0] != n)):
+        size = "" if n is None else f" [{n}]"
+        raise ValueError(f"{name} must be a contiguous int32{size} tensor on {device}")
+
+
 def _as_row_tensor(x, n, device):
     if isinstance(x, (int, float)):
         return torch.full((n,), float(x), dtype=torch.float32, device=device)
@@ -100,7 +125,11 @@ def token_features(logits: torch.Tensor, sampled_ids: torch.Tensor, temperature,
     _check_rows(logits, sampled_ids, temperature, top_p)
     L = _abi.lib()
     code = _dtype_code(logits)
-    out = _alloc_features(n, logits.device) if out is None else out
+    if out is None:
+        out = _alloc_features(n, logits.device)
+    else:
+        _check_features(out, logits.device, n, "out")
+    _check_workspace(workspace, logits.device)
     need = int(L.pr_token_features_workspace(code, n, V, int(top_p is not None)))
     if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
         workspace = torch.empty(need, dtype=torch.uint8, device=logits.device)
@@ -163,6 +192,9 @@ def sample_features(logits: torch.Tensor, temperature, seed: int, offset: int = 
         raise ValueError("logits must be a 2-D CUDA tensor with unit column stride")
     if logits.dtype not in (torch.float32, torch.bfloat16):
         raise ValueError("logits must be float32 or bfloat16")
+    _check_rows(logits, None, temperature, None)
+    if features and out is not None:
+        _check_features(out, logits.device, n, "out")
     ids = torch.empty(n, dtype=torch.int32, device=logits.device) if ids_out is None else ids_out
     if ids.dtype != torch.int32 or ids.shape != (n,) or not ids.is_contiguous() or ids.device != logits.device:
         raise ValueError(f"ids_out must be a contiguous int32 [{n}] tensor on {logits.device}")
@@ -198,6 +230,7 @@ def verifier_head(X: torch.Tensor, offsets: torch.Tensor, weights: torch.Tensor,
         raise ValueError(f"weights must be a contiguous float32 CUDA tensor of {_abi.PR_HEAD_WEIGHTS} entries")
     n = X.shape[0]
     n_req = offsets.shape[0] - 1
+    _check_workspace(workspace, X.device)
     L = _abi.lib()
     need = int(L.pr_verifier_head_workspace(n))
     if need and (workspace is None or workspace.numel() * workspace.element_size() < need):
@@ -244,6 +277,7 @@ def request_aggregate(feats: dict, offsets: torch.Tensor, q: float = 0.1, weight
     if offsets.dtype != torch.int32 or not offsets.is_cuda or offsets.dim() != 1 or not offsets.is_contiguous():
         raise ValueError("offsets must be a contiguous 1-D int32 CUDA tensor")
     n_req = offsets.shape[0] - 1
+    _check_features(feats, offsets.device, None, "feats", ("logprob", "maxprob", "entropy", "margin"))
     out = _alloc_agg(n_req, offsets.device)
     params = _params(q, weights, bias, link)
     st = _abi.lib().pr_request_aggregate(C.byref(_features_struct(feats)), _ptr(offsets), n_req, C.byref(params),
@@ -282,6 +316,9 @@ def calibrate_threshold(scores: torch.Tensor, ship_fraction: float):
 
 def validate_offsets(offsets: torch.Tensor, n_rows: int) -> bool:
     """Synchronous check of an offsets array (``pr_validate_offsets``)."""
+    if not offsets.is_cuda:
+        raise ValueError("offsets must be a CUDA tensor")
+    _check_index_tensor(offsets, "offsets", offsets.device)
     st = _abi.lib().pr_validate_offsets(_ptr(offsets), offsets.shape[0] - 1, n_rows, _stream_handle())
     if st == _abi.PR_ERR_INVALID_ARG:
         return False
@@ -307,10 +344,11 @@ class StreamState:
         n, V = logits.shape
         temperature = _as_row_tensor(temperature, n, logits.device)
         _check_rows(logits, sampled_ids, temperature, None)
-        if slot_ids.dtype != torch.int32 or slot_ids.shape[0] != n:
-            raise ValueError("slot_ids must be int32 [n_active]")
+        _check_index_tensor(slot_ids, "slot_ids", logits.device, n)
         if out is None and want_features:
             out = _alloc_features(n, logits.device)
+        elif out is not None:
+            _check_features(out, logits.device, n, "out")
         fs = C.byref(_features_struct(out)) if out is not None else None
         st = _abi.lib().pr_stream_step(self._h, _ptr(logits), _dtype_code(logits), n, V, logits.stride(0),
                                        _ptr(slot_ids), _ptr(sampled_ids), _ptr(temperature), None, fs,
@@ -319,6 +357,9 @@ class StreamState:
         return out
 
     def finish(self, slots: torch.Tensor, threshold: float) -> dict:
+        if not slots.is_cuda:
+            raise ValueError("slots must be a CUDA tensor")
+        _check_index_tensor(slots, "slots", slots.device)
         n = slots.shape[0]
         out = _alloc_agg(n, slots.device)
         ship = torch.empty(n, dtype=torch.uint8, device=slots.device)
@@ -329,6 +370,9 @@ class StreamState:
         return out
 
     def reset(self, slots: torch.Tensor) -> None:
+        if not slots.is_cuda:
+            raise ValueError("slots must be a CUDA tensor")
+        _check_index_tensor(slots, "slots", slots.device)
         _abi.check("pr_stream_reset_slots",
                    _abi.lib().pr_stream_reset_slots(self._h, _ptr(slots), slots.shape[0], _stream_handle()))
 

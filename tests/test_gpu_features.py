@@ -132,3 +132,48 @@ def test_deterministic():
     one = gpu_features(logits[:1].contiguous(), ids[:1].contiguous(), T[:1].contiguous())  # split path
     for k in ("rank", "argmax", "cutoff", "flags"):
         assert one[k][0] == a1[k][0], k
+
+
+def test_binding_rejects_host_tensors():
+    """Every caller-supplied tensor of the binding must live on the logits'
+    device: a host tensor is refused with ValueError before anything is
+    launched (it would otherwise reach a kernel as a host pointer)."""
+    n, V = 4, 256
+    logits = torch.randn(n, V, device="cuda")
+    ids = torch.zeros(n, dtype=torch.int32, device="cuda")
+    T = torch.ones(n, device="cuda")
+    good = pr.token_features(logits, ids, T)
+    torch.cuda.synchronize()
+    for k in ("lse", "rank", "flags"):
+        bad = dict(good)
+        bad[k] = bad[k].cpu()
+        with pytest.raises(ValueError):
+            pr.token_features(logits, ids, T, out=bad)
+    with pytest.raises(ValueError):
+        pr.token_features(logits, ids, T, top_p=0.9, workspace=torch.empty(1 << 20, dtype=torch.uint8))
+    with pytest.raises(ValueError):
+        pr.sample_features(logits, T.cpu(), seed=1)
+    bad = dict(good)
+    bad["margin"] = bad["margin"].cpu()
+    with pytest.raises(ValueError):
+        pr.sample_features(logits, T, seed=1, out=bad)
+    offsets = torch.tensor([0, 2, n], dtype=torch.int32, device="cuda")
+    with pytest.raises(ValueError):
+        pr.request_aggregate(bad, offsets)
+    with pytest.raises(ValueError):
+        pr.validate_offsets(offsets.cpu(), n)
+    st = pr.StreamState(8, 16)
+    try:
+        with pytest.raises(ValueError):
+            st.step(logits, torch.arange(n, dtype=torch.int32), ids, T)
+        with pytest.raises(ValueError):
+            st.finish(torch.arange(n, dtype=torch.int32), 0.5)
+        with pytest.raises(ValueError):
+            st.reset(torch.arange(n, dtype=torch.int32))
+    finally:
+        st.close()
+    X = torch.zeros(n, 4, device="cuda")
+    w = torch.zeros(pr._abi.PR_HEAD_WEIGHTS, device="cuda")
+    with pytest.raises(ValueError):
+        pr.verifier_head(X, offsets, w, max_len=4, workspace=torch.empty(1 << 16, dtype=torch.uint8))
+    torch.cuda.synchronize()
