@@ -1,4 +1,6 @@
-"""Builds libprouter.so (the HIP kernels and the C ABI) for gfx950 with hipcc.
+"""Builds libprouter.so (the HIP kernels and the C ABI) for gfx950 with hipcc,
+and libprtools.so (the seeded logit generator and the read probe that tests
+and benchmarks use; not part of the verifier's interface).
 
 Usage: python -m paper_2608_28726_amd.build   (or build() from Python)
 """
@@ -17,6 +19,8 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OBJ_DIR = os.path.join(ROOT, "_build", "obj")
 LIB = os.path.join(PKG, "libprouter.so")
+TOOLS_LIB = os.path.join(PKG, "libprtools.so")
+TOOLS_SOURCES = ["tools/prtools.hip"]
 
 SOURCES = ["row_features.hip", "topp.hip", "aggregate.hip", "head.hip", "calibrate.hip", "api.hip"]
 
@@ -45,7 +49,7 @@ def _hipcc() -> str:
 
 
 def _compile(src: str) -> str:
-    obj = os.path.join(OBJ_DIR, os.path.splitext(src)[0] + ".o")
+    obj = os.path.join(OBJ_DIR, os.path.splitext(src)[0].replace("/", "_") + ".o")
     cmd = [_hipcc(), *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
@@ -53,19 +57,25 @@ def _compile(src: str) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    """Compiles every source and links the shared library; returns its path."""
-    os.makedirs(OBJ_DIR, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(4, os.cpu_count() or 1)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
+def _link(objs, lib: str) -> None:
+    tmp = lib + ".tmp"
     cmd = [_hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
-        raise RuntimeError(f"link failed:\n{res.stderr}")
-    os.replace(tmp, LIB)
+        raise RuntimeError(f"link of {os.path.basename(lib)} failed:\n{res.stderr}")
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    """Compiles every source and links both shared libraries; returns the
+    verifier library's path."""
+    os.makedirs(OBJ_DIR, exist_ok=True)
+    with cf.ThreadPoolExecutor(max_workers=min(4, os.cpu_count() or 1)) as ex:
+        objs = list(ex.map(_compile, SOURCES + TOOLS_SOURCES))
+    _link(objs[:len(SOURCES)], LIB)
+    _link(objs[len(SOURCES):], TOOLS_LIB)
     if verbose:
-        print(f"built {LIB}")
+        print(f"built {LIB} and {TOOLS_LIB}")
     return LIB
 
 

@@ -1,0 +1,184 @@
+// Workload tools for tests and benchmarks, built as libprtools.so: the seeded
+// logit-row generator and a read-only HBM bandwidth probe. Neither is part of
+// the verifier's interface (include/prouter.h) and neither computes anything
+// the verifier computes.
+//
+// The generator is the device twin of the numpy generator in
+// paper_2608_28726_amd/workloads.py: both take the same integer and float32
+// steps, so a row generated here and a row generated on the host hold the
+// same bits. That lets expected values be computed on a host from host-made
+// rows and compared with the GPU's outputs on device-made rows.
+//
+// Element v of row r (row key k_r):
+//   k_r  = mix64(seed + (r + 1) * G)                 G = 0x9E3779B97F4A7C15
+//   b    = mix64(k_r + (v + 1) * G)                  64 random bits
+//   g    = normal quantile of b by table (below)
+//   z    = s_r * g        (+ h_r when v == j_r)      float32, one rounding each
+//   bf16 = round-to-nearest-even of z's upper 16 bits (bf16 rows)
+// mix64 is the output function of SplitMix64 (Steele, Lea and Flood,
+// "Fast splittable pseudorandom number generators", OOPSLA 2014), applied to a
+// Weyl sequence, so each element is a pure function of (seed, r, v).
+//
+// The normal quantile is piecewise linear between knots of the exact quantile
+// function Q: the top 16 bits pick a cell [i, i+1) / 2^16 of probability, the
+// next 16 bits the position f / 2^16 inside it, g = A_i + (f * 2^-16) * D_i
+// with A_i = Q(i / 2^16) and D_i = A_{i+1} - A_i (float32). The two outermost
+// cells are refined by a tail table over cells of 2^-32 with the low 32 bits
+// the same way, and the upper tail is the mirror of the lower one. The build
+// compiles with contraction off, so no multiply-add is fused here or in numpy.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace {
+
+constexpr uint64_t kGamma = 0x9E3779B97F4A7C15ull;
+
+__device__ __forceinline__ uint64_t mix64(uint64_t x) {
+  x = (x ^ (x >> 30)) * 0xBF58476D1CE4E5B9ull;
+  x = (x ^ (x >> 27)) * 0x94D049BB133111EBull;
+  return x ^ (x >> 31);
+}
+
+__device__ __forceinline__ float normal_from_bits(uint64_t b, const float2* __restrict__ main_tab,
+                                                  const float2* __restrict__ tail_tab) {
+  const uint32_t hi = static_cast<uint32_t>(b >> 32);
+  const uint32_t cell = hi >> 16;
+  if (cell == 0u || cell == 65535u) {
+    const uint32_t lo = static_cast<uint32_t>(b);
+    const float2 t = tail_tab[lo >> 16];
+    const float g = t.x + (static_cast<float>(lo & 0xffffu) * (1.0f / 65536.0f)) * t.y;
+    return cell == 0u ? g : -g;
+  }
+  const float2 t = main_tab[cell];
+  return t.x + (static_cast<float>(hi & 0xffffu) * (1.0f / 65536.0f)) * t.y;
+}
+
+__device__ __forceinline__ uint32_t bf16_rne(float x) {
+  const uint32_t b = __float_as_uint(x);
+  return (b + 0x7fffu + ((b >> 16) & 1u)) >> 16;
+}
+
+// One thread per 8 consecutive elements of a row.
+template <bool BF16>
+__global__ void __launch_bounds__(256) fill_kernel(void* __restrict__ out, int64_t n_rows, int32_t V,
+                                                   int64_t stride, uint64_t seed, int64_t row0,
+                                                   const int64_t* __restrict__ row_index,
+                                                   const float* __restrict__ s, const float* __restrict__ h,
+                                                   const int64_t* __restrict__ spike,
+                                                   const float2* __restrict__ main_tab,
+                                                   const float2* __restrict__ tail_tab, int vec_ok) {
+  const int64_t per_row = (static_cast<int64_t>(V) + 7) / 8;
+  const int64_t total = n_rows * per_row;
+  const int64_t step = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (int64_t t = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; t < total; t += step) {
+    const int64_t r = t / per_row;
+    const int32_t v0 = static_cast<int32_t>(t - r * per_row) * 8;
+    const int64_t ridx = row_index ? row_index[r] : row0 + r;
+    const uint64_t key = mix64(seed + static_cast<uint64_t>(ridx + 1) * kGamma);
+    const float sr = s[r], hr = h[r];
+    const int64_t jr = spike[r];
+    float z[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int64_t v = v0 + e;
+      const uint64_t b = mix64(key + static_cast<uint64_t>(v + 1) * kGamma);
+      float x = sr * normal_from_bits(b, main_tab, tail_tab);
+      if (v == jr) x = x + hr;
+      z[e] = x;
+    }
+    const int n_here = (V - v0) < 8 ? (V - v0) : 8;
+    if (BF16) {
+      uint16_t* row = static_cast<uint16_t*>(out) + r * stride;
+      if (vec_ok && n_here == 8) {
+        uint4 w;
+        w.x = bf16_rne(z[0]) | (bf16_rne(z[1]) << 16);
+        w.y = bf16_rne(z[2]) | (bf16_rne(z[3]) << 16);
+        w.z = bf16_rne(z[4]) | (bf16_rne(z[5]) << 16);
+        w.w = bf16_rne(z[6]) | (bf16_rne(z[7]) << 16);
+        *reinterpret_cast<uint4*>(row + v0) = w;
+      } else {
+        for (int e = 0; e < n_here; ++e) row[v0 + e] = static_cast<uint16_t>(bf16_rne(z[e]));
+      }
+    } else {
+      float* row = static_cast<float*>(out) + r * stride;
+      if (vec_ok && n_here == 8) {
+        *reinterpret_cast<float4*>(row + v0) = make_float4(z[0], z[1], z[2], z[3]);
+        *reinterpret_cast<float4*>(row + v0 + 4) = make_float4(z[4], z[5], z[6], z[7]);
+      } else {
+        for (int e = 0; e < n_here; ++e) row[v0 + e] = z[e];
+      }
+    }
+  }
+}
+
+typedef uint32_t vec4u __attribute__((ext_vector_type(4)));
+
+// Reads n_vec 16-byte vectors once with nontemporal loads (as the verifier's
+// row kernel reads logits). The running XOR is stored only if it equals a
+// value no real data produces, so the loads cannot be dropped and nothing is
+// written in practice.
+__global__ void __launch_bounds__(256) read_probe_kernel(const vec4u* __restrict__ p, int64_t n_vec,
+                                                         uint32_t* __restrict__ sink) {
+  const int64_t gid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  const int64_t step = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  uint32_t acc = 0;
+  int64_t i = gid;
+  for (; i + 3 * step < n_vec; i += 4 * step) {
+    const vec4u a = __builtin_nontemporal_load(p + i);
+    const vec4u b = __builtin_nontemporal_load(p + i + step);
+    const vec4u c = __builtin_nontemporal_load(p + i + 2 * step);
+    const vec4u d = __builtin_nontemporal_load(p + i + 3 * step);
+    acc ^= a.x ^ a.y ^ a.z ^ a.w ^ b.x ^ b.y ^ b.z ^ b.w ^ c.x ^ c.y ^ c.z ^ c.w ^ d.x ^ d.y ^ d.z ^ d.w;
+  }
+  for (; i < n_vec; i += step) {
+    const vec4u a = __builtin_nontemporal_load(p + i);
+    acc ^= a.x ^ a.y ^ a.z ^ a.w;
+  }
+  if (acc == 0x9E3779B9u) sink[gid] = acc;
+}
+
+}  // namespace
+
+extern "C" {
+
+// Fills rows [n_rows][row_stride] (dtype 0 float32, 1 bfloat16) with the rows
+// described above. Row r uses key index row_index[r] when row_index is not
+// NULL, else row0 + r. s, h (float32) and spike (int64; outside [0, V) means
+// no spike) are device arrays of n_rows entries; main_tab and tail_tab are
+// device float2[65536] tables (A_i, D_i). Returns 0, 1 (bad argument) or 3
+// (launch failure).
+int prt_fill_logits(void* out, int dtype, int64_t n_rows, int32_t V, int64_t row_stride, uint64_t seed,
+                    int64_t row0, const int64_t* row_index, const float* s, const float* h, const int64_t* spike,
+                    const void* main_tab, const void* tail_tab, void* stream) {
+  if ((dtype != 0 && dtype != 1) || n_rows < 0 || V < 1 || row_stride < V) return 1;
+  if (n_rows == 0) return 0;
+  if (!out || !s || !h || !spike || !main_tab || !tail_tab) return 1;
+  const size_t esz = dtype == 1 ? 2 : 4;
+  const int vec_ok = (reinterpret_cast<uintptr_t>(out) % 16 == 0) && ((row_stride * esz) % 16 == 0);
+  const int64_t total = n_rows * ((static_cast<int64_t>(V) + 7) / 8);
+  int64_t blocks = (total + 255) / 256;
+  if (blocks > 65536) blocks = 65536;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const float2* mt = static_cast<const float2*>(main_tab);
+  const float2* tt = static_cast<const float2*>(tail_tab);
+  if (dtype == 1)
+    hipLaunchKernelGGL(fill_kernel<true>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, out, n_rows, V,
+                       row_stride, seed, row0, row_index, s, h, spike, mt, tt, vec_ok);
+  else
+    hipLaunchKernelGGL(fill_kernel<false>, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, st, out, n_rows, V,
+                       row_stride, seed, row0, row_index, s, h, spike, mt, tt, vec_ok);
+  return hipGetLastError() == hipSuccess ? 0 : 3;
+}
+
+// Launches the read probe over nbytes (a multiple of 16) at buf (16-byte
+// aligned) with `blocks` workgroups of 256 threads. sink is a device array of
+// blocks * 256 uint32 that is written only in the case described above.
+int prt_read_probe(const void* buf, int64_t nbytes, uint32_t* sink, int32_t blocks, void* stream) {
+  if (!buf || !sink || nbytes <= 0 || nbytes % 16 != 0 || blocks <= 0) return 1;
+  if (reinterpret_cast<uintptr_t>(buf) % 16 != 0) return 1;
+  hipLaunchKernelGGL(read_probe_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
+                     static_cast<hipStream_t>(stream), static_cast<const vec4u*>(buf), nbytes / 16, sink);
+  return hipGetLastError() == hipSuccess ? 0 : 3;
+}
+
+}  // extern "C"

@@ -24,14 +24,6 @@ def _batch_on_gpu(w, lengths=None):
     return b, logits, ids, T, P
 
 
-def test_pr1_reference_config_all_rows():
-    """8 requests x 64 tokens, V = 32,000 float32: every row."""
-    w = wl.WORKLOADS["pr1_ref_8x64_v32000_f32"]
-    b, logits, ids, T, _ = _batch_on_gpu(w)
-    print(f"case pr1_ref rows={b.n_rows} V={w.V}", flush=True)
-    compare_features(gpu_features(logits, ids, T), oracle_features(logits, ids, T))
-
-
 def test_ragged_bf16_rows_scaled():
     """The ragged-batch row model (V = 151,936 bf16, T = 0.7) on a few requests."""
     w = wl.scaled(wl.WORKLOADS["ragged_64req_v151936_bf16"], n_req=5, len_hi=20)
