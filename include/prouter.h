@@ -205,9 +205,10 @@ pr_status pr_feature_sequence(const void* logits, pr_dtype dtype, int64_t n_rows
  *              float32 rounding of the masses (relative 1e-6).
  *   features   host pointer to a struct of device arrays (all members set),
  *              or NULL: the per-token features of pr_token_features for the
- *              drawn token, except rank, which is written as 0 (counting
- *              the tokens above y needs z_y before the pass); a row with y =
- *              -1 is flagged PR_FLAG_BAD_ID besides its other flags.
+ *              drawn token, except rank, which is written as -1 ("not
+ *              available", as for a bad id: counting the tokens above y
+ *              needs z_y before the pass); a row with y = -1 is flagged
+ *              PR_FLAG_BAD_ID besides its other flags.
  *   offsets, n_req, top_k, X
  *              X NULL: not computed. Otherwise the paper's verifier input
  *              sequence for the drawn tokens, with the arguments and layout

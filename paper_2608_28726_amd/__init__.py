@@ -179,7 +179,7 @@ def sample_features(logits: torch.Tensor, temperature, seed: int, offset: int = 
 
     Returns ``(ids, feats, X)``: the drawn tokens (int32 [n_rows], -1 where the
     distribution is undefined), the per-token features for them as
-    :func:`token_features` returns them (rank written as 0), or None with
+    :func:`token_features` returns them (rank written as -1, not available), or None with
     ``features=False``, and the paper's input sequence X for them when
     ``offsets`` is given (else None). The draw is a fixed function of
     (seed, offset, row index, logits, temperature) and of the workgroup size

@@ -96,7 +96,7 @@ void row_features_kernel(RowArgs a) {
   RowCtx cf = cx;  // the context the row is finalised with
   if constexpr (SAMPLE) {
     // The token drawn for the row; its rank is not counted (that needs its
-    // value before the pass), and is written as 0.
+    // value before the pass), and is written as -1, "not available".
     __shared__ sample::Shared ssh;
     __shared__ float sh_ref;
     __shared__ uint32_t sh_def;
@@ -120,7 +120,7 @@ void row_features_kernel(RowArgs a) {
         write_sequence_row(a, r, conf, flags, H, rho);
         if (SAMPLE) {
           a.sampled_out[r] = cf.y;
-          if (a.out.rank) a.out.rank[r] = 0;
+          if (a.out.rank) a.out.rank[r] = -1;
         }
       }
     }
@@ -134,7 +134,7 @@ void row_features_kernel(RowArgs a) {
       stream_update(a.st, kEarlySlot ? ss : slot_load(a, r), conf);
       if (SAMPLE) {
         a.sampled_out[r] = cf.y;
-        if (a.out.rank) a.out.rank[r] = 0;
+        if (a.out.rank) a.out.rank[r] = -1;
       }
     }
     if (pm.slot >= 0) p2::feed_row(a, pm, conf);

@@ -147,9 +147,9 @@ def test_features_and_sequence_for_drawn_tokens():
     y = ids.cpu().numpy()
     assert ((y >= 0) & (y < w.V)).all()
     g = {k: v.cpu().numpy() for k, v in feats.items()}
-    assert (g["rank"] == 0).all()
+    assert (g["rank"] == -1).all()  # "not available" on the fused path
     o = oracle_features(logits, ids, T)
-    g["rank"] = o["rank"].copy()  # not computed on the fused path
+    g["rank"] = o["rank"].copy()
     compare_features(g, o, what="drawn ")
     H = oseq.topk_entropy_batch(wl.to_host_raw(b.logits), dtype_name(logits), b.temperature.numpy())
     Xo = oseq.feature_sequence(o, H, b.offsets)
@@ -238,5 +238,6 @@ def test_full_size_draws_are_consistent():
     o = oracle.token_features_batch(wl.to_host_raw(b.logits[sel]), "bf16", ids[sel].cpu().numpy(),
                                     b.temperature[sel].cpu().numpy())
     g = {k: v.cpu().numpy()[rows] for k, v in feats.items()}
+    assert (g["rank"] == -1).all()
     g["rank"] = o["rank"].copy()
     compare_features(g, o, what="full-size drawn ")
