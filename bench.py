@@ -245,13 +245,15 @@ def read_probe(torch, wl, buffers, reps=4):
     L = wl.tools()
     stream = torch.cuda.current_stream()
     best = None
-    for blocks in (1024, 2048, 4096, 8192):
+    for blocks, unroll in ((2048, 4), (4096, 4), (8192, 4), (16384, 4), (2048, 8), (4096, 8), (8192, 8),
+                           (2048, 16), (4096, 16)):
         sink = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda")
         nb = [(b.numel() * b.element_size()) // 16 * 16 for b in buffers]
 
         def launch(k):
             st = L.prt_read_probe(ctypes.c_void_p(buffers[k % len(buffers)].data_ptr()), nb[k % len(buffers)],
-                                  ctypes.c_void_p(sink.data_ptr()), blocks, ctypes.c_void_p(stream.cuda_stream))
+                                  ctypes.c_void_p(sink.data_ptr()), blocks, unroll,
+                                  ctypes.c_void_p(stream.cuda_stream))
             if st != 0:
                 raise RuntimeError(f"prt_read_probe failed with status {st}")
         launch(0)
@@ -267,7 +269,9 @@ def read_probe(torch, wl, buffers, reps=4):
         gbs = nbytes / (ms * 1e-3) / 1e9
         if best is None or gbs > best["gb_per_s"]:
             best = {"gb_per_s": gbs, "bytes_per_launch": nbytes, "ms": ms, "blocks": blocks,
-                    "kernel": "read_probe_kernel (nontemporal 16-byte loads, 256 threads per workgroup)"}
+                    "loads_in_flight_per_thread": unroll,
+                    "kernel": "read_probe_kernel (nontemporal 16-byte loads, 256 threads per workgroup; "
+                              "best of 9 grid shapes)"}
     return best
 
 
@@ -589,7 +593,8 @@ def main():
     traffic = stored_traffic(args.traffic_json, w.name, args.path)
     probe = read_probe(torch, wl, extra.pop("_probe_buffers"))
     probe["frac_of_probe"] = achieved / probe["gb_per_s"]
-    log(f"[bench] read probe {probe['gb_per_s']:.0f} GB/s ({probe['blocks']} workgroups); the kernel reaches "
+    log(f"[bench] read probe {probe['gb_per_s']:.0f} GB/s ({probe['blocks']} workgroups, "
+        f"{probe['loads_in_flight_per_thread']} loads in flight); the kernel reaches "
         f"{100 * probe['frac_of_probe']:.1f} % of it")
 
     result = {

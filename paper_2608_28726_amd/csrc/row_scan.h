@@ -124,8 +124,14 @@ __device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx&
 
     // Sum of 2^x and of 2^x * x. A masked logit (-inf) has x = -inf and
     // 2^x = 0; x is clamped to a finite value so that 0 * x stays 0.
+    // The step's terms are summed on their own first and the step sums then
+    // join the lane's sums: a lane that holds a term near 1 (the row's
+    // maximum) would otherwise round away every term below 2^-24 added after
+    // it, which in a near one-hot row (a spike 20 nats above the rest) is
+    // most of S - 1 and makes log-prob err by 1e-5.
     const float na = -L.a;
     float ev[NV * VEC];
+    float s0 = 0.0f, s1 = 0.0f, q0 = 0.0f, q1 = 0.0f;
 #pragma unroll
     for (int k = 0; k < NV * VEC; k += 2) {
       const float x0 = fmaf(z[k], cx.c, na);
@@ -134,11 +140,22 @@ __device__ __forceinline__ void consume(const vec4u* v, int64_t i, const RowCtx&
       const float e1 = fast_exp2(x1);
       ev[k] = e0;
       ev[k + 1] = e1;
-      L.S0 += e0;
-      L.S1 += e1;
-      L.E0 = fmaf(e0, fmaxf(x0, -kBig), L.E0);
-      L.E1 = fmaf(e1, fmaxf(x1, -kBig), L.E1);
+      if (k == 0) {
+        s0 = e0;
+        s1 = e1;
+        q0 = e0 * fmaxf(x0, -kBig);
+        q1 = e1 * fmaxf(x1, -kBig);
+      } else {
+        s0 += e0;
+        s1 += e1;
+        q0 = fmaf(e0, fmaxf(x0, -kBig), q0);
+        q1 = fmaf(e1, fmaxf(x1, -kBig), q1);
+      }
     }
+    L.S0 += s0;
+    L.S1 += s1;
+    L.E0 += q0;
+    L.E1 += q1;
     hook.step(z, ev, cmax, i, L);
   }
 

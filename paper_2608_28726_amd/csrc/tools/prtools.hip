@@ -114,21 +114,22 @@ __global__ void __launch_bounds__(256) fill_kernel(void* __restrict__ out, int64
 typedef uint32_t vec4u __attribute__((ext_vector_type(4)));
 
 // Reads n_vec 16-byte vectors once with nontemporal loads (as the verifier's
-// row kernel reads logits). The running XOR is stored only if it equals a
-// value no real data produces, so the loads cannot be dropped and nothing is
-// written in practice.
+// row kernel reads logits), UNROLL loads in flight per thread. The running XOR
+// is stored only if it equals a value no real data produces, so the loads
+// cannot be dropped and nothing is written in practice.
+template <int UNROLL>
 __global__ void __launch_bounds__(256) read_probe_kernel(const vec4u* __restrict__ p, int64_t n_vec,
                                                          uint32_t* __restrict__ sink) {
   const int64_t gid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   const int64_t step = static_cast<int64_t>(gridDim.x) * blockDim.x;
   uint32_t acc = 0;
   int64_t i = gid;
-  for (; i + 3 * step < n_vec; i += 4 * step) {
-    const vec4u a = __builtin_nontemporal_load(p + i);
-    const vec4u b = __builtin_nontemporal_load(p + i + step);
-    const vec4u c = __builtin_nontemporal_load(p + i + 2 * step);
-    const vec4u d = __builtin_nontemporal_load(p + i + 3 * step);
-    acc ^= a.x ^ a.y ^ a.z ^ a.w ^ b.x ^ b.y ^ b.z ^ b.w ^ c.x ^ c.y ^ c.z ^ c.w ^ d.x ^ d.y ^ d.z ^ d.w;
+  for (; i + (UNROLL - 1) * step < n_vec; i += UNROLL * step) {
+    vec4u v[UNROLL];
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) v[u] = __builtin_nontemporal_load(p + i + u * step);
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
   }
   for (; i < n_vec; i += step) {
     const vec4u a = __builtin_nontemporal_load(p + i);
@@ -171,13 +172,23 @@ int prt_fill_logits(void* out, int dtype, int64_t n_rows, int32_t V, int64_t row
 }
 
 // Launches the read probe over nbytes (a multiple of 16) at buf (16-byte
-// aligned) with `blocks` workgroups of 256 threads. sink is a device array of
-// blocks * 256 uint32 that is written only in the case described above.
-int prt_read_probe(const void* buf, int64_t nbytes, uint32_t* sink, int32_t blocks, void* stream) {
+// aligned) with `blocks` workgroups of 256 threads and `unroll` (4, 8 or 16)
+// loads in flight per thread. sink is a device array of blocks * 256 uint32
+// that is written only in the case described above.
+int prt_read_probe(const void* buf, int64_t nbytes, uint32_t* sink, int32_t blocks, int32_t unroll, void* stream) {
   if (!buf || !sink || nbytes <= 0 || nbytes % 16 != 0 || blocks <= 0) return 1;
   if (reinterpret_cast<uintptr_t>(buf) % 16 != 0) return 1;
-  hipLaunchKernelGGL(read_probe_kernel, dim3(static_cast<unsigned>(blocks)), dim3(256), 0,
-                     static_cast<hipStream_t>(stream), static_cast<const vec4u*>(buf), nbytes / 16, sink);
+  const vec4u* p = static_cast<const vec4u*>(buf);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const dim3 grid(static_cast<unsigned>(blocks));
+  if (unroll == 4)
+    hipLaunchKernelGGL(read_probe_kernel<4>, grid, dim3(256), 0, st, p, nbytes / 16, sink);
+  else if (unroll == 8)
+    hipLaunchKernelGGL(read_probe_kernel<8>, grid, dim3(256), 0, st, p, nbytes / 16, sink);
+  else if (unroll == 16)
+    hipLaunchKernelGGL(read_probe_kernel<16>, grid, dim3(256), 0, st, p, nbytes / 16, sink);
+  else
+    return 1;
   return hipGetLastError() == hipSuccess ? 0 : 3;
 }
 

@@ -37,6 +37,19 @@ def float_mismatch(gpu, ref, atol=ATOL, rtol=RTOL) -> np.ndarray:
     return ~(ok | both_nan)
 
 
+def tolerance_ratio(gpu, ref, mask=None, atol=ATOL, rtol=RTOL) -> float:
+    """Largest |gpu - oracle| / (atol + rtol |oracle|) over the finite pairs
+    (1.0 is the edge of the tolerance)."""
+    g = np.asarray(gpu, dtype=np.float64)
+    o = np.asarray(ref, dtype=np.float64)
+    ok = np.isfinite(g) & np.isfinite(o)
+    if mask is not None:
+        ok &= mask
+    if not ok.any():
+        return 0.0
+    return float(np.max(np.abs(g[ok] - o[ok]) / (atol + rtol * np.abs(o[ok]))))
+
+
 def assert_floats(name, gpu, ref, mask=None, atol=ATOL, rtol=RTOL):
     bad = float_mismatch(gpu, ref, atol, rtol)
     if mask is not None:

@@ -18,7 +18,7 @@ import torch
 
 import paper_2608_28726_amd as pr
 from paper_2608_28726_amd import workloads as wl
-from tests.helpers import ROOT, assert_floats, assert_ints, decisions_agree
+from tests.helpers import ROOT, assert_floats, assert_ints, decisions_agree, tolerance_ratio
 from tests.gpu_common import require_gpu
 
 pytestmark = pytest.mark.gpu
@@ -45,8 +45,12 @@ def load(name):
 def compare_rows(f: dict, g: dict, what: str, sel=slice(None)):
     """Element-wise parity of per-row outputs f (GPU, numpy) with stored ones."""
     amb = g["ambiguous"][sel]
+    ratios = {}
     for k in FLOATS:
-        assert_floats(f"{what} {k}", f[k], g[k][sel], mask=~amb if k in NUCLEUS_DEPENDENT else None)
+        mask = ~amb if k in NUCLEUS_DEPENDENT else None
+        ratios[k] = tolerance_ratio(f[k], g[k][sel], mask)
+        assert_floats(f"{what} {k}", f[k], g[k][sel], mask=mask)
+    print(f"  {what}: worst error / tolerance " + ", ".join(f"{k} {v:.3f}" for k, v in ratios.items()), flush=True)
     for k in ("rank", "argmax"):
         assert_ints(f"{what} {k}", f[k], g[k][sel])
     assert_ints(f"{what} cutoff", f["cutoff"], g["cutoff"][sel], mask=~amb)
