@@ -520,11 +520,219 @@ __device__ Nucleus legacy_nucleus(const void* row, int32_t V, int64_t h, int64_t
   return nuc;
 }
 
-// The nucleus from the stats-pass histogram and one exact pass. Returns
-// false (and leaves nuc unset) when the row must take the three-pass method.
+// Lanes of a workgroup that may re-read their whole stretch in the sparse
+// exact pass (a lane with three or more buckets reaching the window); with
+// more, the row takes the dense pass.
+constexpr uint32_t kSparseFullLanes = 16;
+// Bound on the relative error of a bin's mass as estimated from its count
+// and offset sum (first order around the centre), per logit: the second-order
+// term (|x| <= 0.5 bin + 2.5e-4 bin of float32 rounding of the coordinate,
+// at 0.0183 nats per bin) is below 4.24e-5 of the centre's mass, the
+// quantised offsets and the coordinate's rounding add 6.7e-6; 5.5e-5 keeps a
+// margin (the exact map from the float32 coordinate to nats is used).
+constexpr double kBinMassRelErr = 5.5e-5;
+
+// The window of bins around P of the total, located from the histogram.
+struct Window {
+  int b_lo, b_hi;       // bins of the window (-1: the list above the bins)
+  uint32_t above;       // logits above the window (exact, from the counts and the list)
+  uint32_t inwin;       // logits in the window (exact)
+  double s_below;       // estimated mass of the bins below the window (relative to M)
+  double s_below_err;   // bound on the error of s_below
+};
+
+// Calls fn(z) for the logits of the row that the sparse exact pass reads:
+// every scalar head/tail logit, the lane's whole stretch when `full`, else
+// the buckets (U = 2 vectors each) starting at vector indices s1 and s2
+// (-1: none). Unread vectors cannot hold a logit at or above the window.
+template <typename Tin, typename Fn>
+__device__ __forceinline__ void for_each_listed_logit(const void* row, int32_t V, int64_t h, int64_t nvec, bool full,
+                                                      int64_t s1, int64_t s2, Fn fn) {
+  constexpr int VEC = Elem<Tin>::kVec;
+  const int t = threadIdx.x;
+  if (t < h) fn(Elem<Tin>::load1(row, t));
+  for (int64_t e = h + nvec * VEC + t; e < V; e += kTpBlock) fn(Elem<Tin>::load1(row, e));
+  const vec4u* vp = reinterpret_cast<const vec4u*>(static_cast<const Tin*>(row) + h);
+  auto body = [&](const vec4u& x) {
+    float z[VEC];
+    Elem<Tin>::unpack(x, z);
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) fn(z[k]);
+  };
+  if (full) {
+    int64_t v = t;
+    for (; v + kTpBlock < nvec; v += 2 * kTpBlock) {
+      const vec4u x0 = load_stream(vp + v);
+      const vec4u x1 = load_stream(vp + v + kTpBlock);
+      body(x0);
+      body(x1);
+    }
+    if (v < nvec) body(load_stream(vp + v));
+    return;
+  }
+  const int64_t idx[4] = {s1, s1 + kTpBlock, s2, s2 + kTpBlock};
+  vec4u x[4];
+  bool ok[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    ok[u] = (u < 2 ? s1 : s2) >= 0 && idx[u] < nvec;
+    x[u] = ok[u] ? load_stream(vp + idx[u]) : neg_inf_vec<Tin>();
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+    if (ok[u]) body(x[u]);
+}
+
+// Steps 2 and 3 of the histogram method: the exact pass over the row (dense)
+// or over the buckets that can reach the window (sparse), the window sorted
+// and scanned. Dense: S is the float64 total over every binned logit.
+// Sparse: S is the exact mass at or above the window plus the histogram's
+// estimate of the mass below it, whose error is bounded; the cutoff is taken
+// only where the whole uncertainty interval of P * S leads to the same index,
+// and the logits read must account for every counted logit at or above the
+// window. Returns false when the method cannot decide (the caller then tries
+// the dense pass, then the three-pass method).
+template <typename Tin, bool SPARSE>
+__device__ bool exact_cut(const void* row, int32_t V, int64_t h, int64_t nvec, const Dist& D, float P,
+                          const HistHook& hk, TpShared& sh, const Window& W, double c0, double invK, bool full,
+                          int64_t s1, int64_t s2, Nucleus& nuc) {
+  const double* tab = sh.exptab;
+  const int b_lo = W.b_lo, b_hi = W.b_hi;
+  if (threadIdx.x == 0) sh.wcount = 0;
+  __syncthreads();
+  // 2. exact pass: sums above the window, the window gathered, the total
+  // (every binned logit: those more than 50 nats below M add less than
+  // V e^-50 of S). With u = (z - M) / T - c0 by one fma (the row constant
+  // -M / T - c0 is rounded once: a common factor of every mass, which the
+  // cutoff test does not see), a logit of bin b sits r = u + b / kHK from
+  // its bin centre and dd = u + c0 nats below M; the entropy sum above the
+  // window is taken as sum e u + c0 * sum e.
+  double mA = 0.0, eAu = 0.0, sT = 0.0;
+  uint32_t nA = 0;
+  const double nMTc = -static_cast<double>(D.M) * D.invT64 - c0;
+  auto visit = [&](float z) {
+    const float bf = fmaf(z, hk.kz, hk.k0);
+    if (!(bf < static_cast<float>(kHB))) return;  // beyond 50 nats below A0, -inf, NaN
+    int b;
+    if (bf >= 0.0f) {
+      b = static_cast<int>(bf);
+      if (SPARSE && b > b_hi) return;  // below the window: estimated from the histogram
+    } else {
+      b = -1;  // the list above the bins
+    }
+    const double u = fma(static_cast<double>(z), D.invT64, nMTc);
+    double e;
+    if (b >= 0) {
+      const double r = fma(static_cast<double>(b), invK, u);
+      const float rf = static_cast<float>(r);
+      const float cf = fmaf(rf, fmaf(rf, 1.0f / 120.0f, 1.0f / 24.0f), 1.0f / 6.0f);
+      double q = fma(static_cast<double>(cf), r, 0.5);
+      q = fma(q, r, 1.0);
+      q = fma(q, r, 1.0);
+      e = sh.u.wtab[b] * q;
+    } else {
+      e = exp_tang(fmax(u + c0, -700.0), tab);
+    }
+    if (!SPARSE) sT += e;
+    if (b < b_lo) {  // above the window (lanes outside it keep their sums as they are)
+      mA += e;
+      eAu = fma(e, u, eAu);
+      if (SPARSE) ++nA;
+    } else if (b <= b_hi) {
+      const uint32_t slot = atomicAdd(&sh.wcount, 1u);
+      if (slot < static_cast<uint32_t>(kCap)) sh.win[slot] = z;
+    }
+  };
+  if (SPARSE)
+    for_each_listed_logit<Tin>(row, V, h, nvec, full, s1, s2, visit);
+  else
+    for_each_logit<Tin>(row, V, h, nvec, visit);
+  block_sum2(mA, eAu, sh);
+  const double eA = fma(c0, mA, eAu);
+  double sT2 = sT, unused = 0.0;
+  if (!SPARSE) block_sum2(sT2, unused, sh);
+  const uint32_t cA = W.above;
+  const uint32_t nw_all = sh.wcount;
+  if (nw_all > static_cast<uint32_t>(kCap)) return false;
+  if (SPARSE) {  // every counted logit at or above the window was read
+    const uint32_t nA_all = block_sum_u(nA, sh);
+    if (nA_all != cA || nw_all != W.inwin) return false;
+  }
+
+  // 3. sort the window (descending), scan its masses, verify the crossing
+  const int nw = static_cast<int>(nw_all);
+  int n2 = 2;
+  while (n2 < nw) n2 <<= 1;
+  for (int i = nw + threadIdx.x; i < n2; i += kTpBlock) sh.win[i] = -INFINITY;
+  __syncthreads();
+  bitonic_desc(sh.win, n2);
+  const int per = (n2 + kTpBlock - 1) / kTpBlock;
+  const int i0 = threadIdx.x * per;
+  const int i1 = i0 + per < nw ? i0 + per : nw;
+  double sm = 0.0, se = 0.0;
+  for (int i = i0; i < i1; ++i) {
+    const double dd = D.d64(sh.win[i]);
+    const double e = exp_tang(dd, tab);
+    sm += e;
+    se += e * dd;
+  }
+  const double cm = block_exclusive_scan(sm, sh);
+  const double ce = block_exclusive_scan(se, sh);
+  double wm = sm, we = se;
+  block_sum2(wm, we, sh);
+  // The total and the range the target P * S may lie in: exact (to float64
+  // rounding) in the dense pass, the histogram estimate's bound in the sparse one.
+  const double S = SPARSE ? mA + wm + W.s_below : sT2;
+  const double err = SPARSE ? W.s_below_err + 1e-13 * S : 0.0;
+  const double t_lo = static_cast<double>(P) * (S - err);
+  const double t_hi = static_cast<double>(P) * (S + err);
+  if (!(mA < t_lo) || mA + wm < t_hi) return false;  // crossing outside the window
+  if (threadIdx.x == 0) {
+    sh.jfirst = 0xffffffffu;
+    sh.rdigit = 0xffffffffu;  // the first index reaching t_hi
+  }
+  __syncthreads();
+  double run_m = mA + cm;
+  bool lo_found = false;
+  for (int i = i0; i < i1; ++i) {
+    run_m += exp_tang(D.d64(sh.win[i]), tab);
+    if (!lo_found && run_m >= t_lo) {
+      atomicMin(&sh.jfirst, static_cast<uint32_t>(i));
+      lo_found = true;
+    }
+    if (run_m >= t_hi) {
+      atomicMin(&sh.rdigit, static_cast<uint32_t>(i));
+      break;
+    }
+  }
+  __syncthreads();
+  const uint32_t jf = sh.jfirst;
+  if (jf == 0xffffffffu || jf != sh.rdigit) return false;  // not decided within the bound
+  if (static_cast<int>(jf) >= i0 && static_cast<int>(jf) < i1) {
+    double m2 = mA + cm, e2 = eA + ce;
+    for (int i = i0; i <= static_cast<int>(jf); ++i) {
+      const double dd = D.d64(sh.win[i]);
+      const double e = exp_tang(dd, tab);
+      m2 += e;
+      e2 += e * dd;
+    }
+    sh.SN = m2;
+    sh.EN = e2;
+  }
+  __syncthreads();
+  nuc.k = static_cast<int32_t>(cA + jf + 1);
+  nuc.S = sh.SN;
+  nuc.E = sh.EN;
+  return true;
+}
+
+// The nucleus from the stats-pass histogram and one exact pass (sparse when
+// few buckets can reach the window, else dense). Returns false (and leaves
+// nuc unset) when the row must take the three-pass method. tk holds each
+// lane's three largest bucket maxima and the steps of the first two.
 template <typename Tin>
 __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec, const Dist& D, float P,
-                             float A0, const HistHook& hk, TpShared& sh, Nucleus& nuc) {
+                             float A0, const HistHook& hk, const topk::Hook& tk, TpShared& sh, Nucleus& nuc) {
   const double* tab = sh.exptab;
   const uint32_t n_above = sh.n_above;
   if (n_above > static_cast<uint32_t>(kAboveCap)) return false;
@@ -536,24 +744,28 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   // (beyond about 4,800) take the three-pass method.
   if (!(fabsf(hk.k0) < 0x1p18f)) return false;
 
-  // 1. the window of bins around P * (total): a logit of bin b lies at
-  // (b + 1/2 + delta) / kHK - kHAbove nats below A0; with w = 1/kHK the bin's
-  // mass is mass(centre) * sum exp(-delta w) ~ mass(centre) * (count - w *
-  // sum delta) (second-order error below count * w^2 / 8). Masses relative
-  // to M.
-  const double lead = (static_cast<double>(A0) - static_cast<double>(D.M)) * D.invT64 + kHAbove;
+  // 1. the window of bins around P * (total). bf = z kz + k0 (the float32
+  // constants, exactly) is a logit's coordinate: it lies (M - z) / T =
+  // bf * hb - lead nats below M, with hb = -1 / (kz T) and lead = -(M + k0 /
+  // kz) / T, so that the only error of the rounded coordinate is its last
+  // rounding. A bin's mass is taken at its centre, corrected to first order
+  // by the offsets: w_b (count - hb * sum of offsets) with w_b the mass at
+  // the centre (relative error below kBinMassRelErr per logit).
+  const double hb = -D.invT64 / static_cast<double>(hk.kz);
+  const double lead = -(static_cast<double>(D.M) + static_cast<double>(hk.k0) / static_cast<double>(hk.kz)) * D.invT64;
   const double invK = 1.0 / static_cast<double>(kHK);
   // Kept compact (it runs once per row): the loops over a thread's kPer bins
   // are not unrolled (one copy of the float64 exp each; the second loop
   // recomputes the masses of the first), and the crossing bins are found
   // with a ballot and one LDS atomic per wave.
+  auto centre_mass = [&](int b) -> double { return exp(fma(-(static_cast<double>(b) + 0.5), hb, lead)); };
   auto bin_mass = [&](int b) -> double {
-    const double w = exp(fma(-(static_cast<double>(b) + 0.5), invK, lead));
+    const double w = centre_mass(b);
     const uint64_t word = sh.u.hs.bins[b];
     const double cnt = static_cast<double>(static_cast<uint32_t>(word >> kCountShift));
     const double dsum =
         (static_cast<double>(word & ((uint64_t{1} << kCountShift) - 1)) - cnt * (0.5 * kOffQ)) * (1.0 / kOffQ);
-    return fma(-dsum, invK, cnt) * w;
+    return fma(-dsum, hb, cnt) * w;
   };
   double sa = 0.0;
   for (uint32_t i = threadIdx.x; i < n_above; i += kTpBlock) sa += exp_tang(D.d64(sh.above[i]), tab);
@@ -594,21 +806,31 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
       if (m_hi) atomicMin(&sh.hb_hi, f_hi);
     }
   }
-  if (threadIdx.x == 0) sh.wcount = 0;
   __syncthreads();
-  const int b_lo = sa >= t_lo ? -1 : sh.hb_lo;  // -1: the list above the bins
-  const int b_hi = sa >= t_hi ? -1 : sh.hb_hi;
+  Window W;
+  W.b_lo = sa >= t_lo ? -1 : sh.hb_lo;  // -1: the list above the bins
+  W.b_hi = sa >= t_hi ? -1 : sh.hb_hi;
   uint32_t inwin = 0, above = 0;
+  double sb = 0.0, sb_max = 0.0;
 #pragma unroll 1
   for (int k = 0; k < kPer; ++k) {
     const int b = b0 + k;
     const uint32_t cnt = static_cast<uint32_t>(sh.u.hs.bins[b] >> kCountShift);
-    if (b < b_lo) above += cnt;
-    else if (b <= b_hi) inwin += cnt;
+    if (b < W.b_lo) {
+      above += cnt;
+    } else if (b <= W.b_hi) {
+      inwin += cnt;
+    } else if (cnt) {  // below the window: the estimate and a bound on its error
+      sb += bin_mass(b);
+      sb_max += static_cast<double>(cnt) * centre_mass(b);
+    }
   }
-  inwin = block_sum_u(inwin, sh) + (b_lo < 0 ? n_above : 0u);
-  above = block_sum_u(above, sh) + (b_lo >= 0 ? n_above : 0u);  // counts are exact
-  if (inwin > static_cast<uint32_t>(kCap)) return false;
+  W.inwin = block_sum_u(inwin, sh) + (W.b_lo < 0 ? n_above : 0u);
+  W.above = block_sum_u(above, sh) + (W.b_lo >= 0 ? n_above : 0u);  // counts are exact
+  block_sum2(sb, sb_max, sh);
+  W.s_below = sb;
+  W.s_below_err = kBinMassRelErr * 1.01 * sb_max;  // 1.01: a logit's mass is below 1.0093 w_b
+  if (W.inwin > static_cast<uint32_t>(kCap)) return false;
   // The counts are consumed: the same LDS now holds exp(centre of bin b - M).
   // A logit of bin b is exp(dd) = wtab[b] * exp(r), r = dd - centre, |r| at
   // most half a bin (0.0092 nats) plus the float32 rounding of bf (see
@@ -616,109 +838,23 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   // = 1/6 + r/24 + r^2/120 taken in float32 (its rounding, below 1.5e-8,
   // moves the polynomial by less than |r|^3 1.5e-8 < 3e-14). The list
   // takes the table-driven exp.
-  const double c0 = lead - 0.5 * invK;  // centre of bin b: c0 - b * invK
+  const double lead0 = (static_cast<double>(A0) - static_cast<double>(D.M)) * D.invT64 + kHAbove;
+  const double c0 = lead0 - 0.5 * invK;  // centre of bin b: c0 - b * invK
 #pragma unroll 1
   for (int k = 0; k < kPer; ++k) sh.u.wtab[b0 + k] = exp(fma(-static_cast<double>(b0 + k), invK, c0));
   __syncthreads();
 
-  // 2. exact pass: sums above the window, the window gathered, the total
-  // (every binned logit: those more than 50 nats below M add less than
-  // V e^-50 of S). With u = (z - M) / T - c0 by one fma (the row constant
-  // -M / T - c0 is rounded once: a common factor of every mass, which the
-  // cutoff test does not see), a logit of bin b sits r = u + b / kHK from
-  // its bin centre and dd = u + c0 nats below M; the entropy sum above the
-  // window is taken as sum e u + c0 * sum e.
-  double mA = 0.0, eAu = 0.0, sT = 0.0;
-  const double nMTc = -static_cast<double>(D.M) * D.invT64 - c0;
-  for_each_logit<Tin>(row, V, h, nvec, [&](float z) {
-    const float bf = fmaf(z, hk.kz, hk.k0);
-    if (!(bf < static_cast<float>(kHB))) return;  // beyond 50 nats below A0, -inf, NaN
-    const double u = fma(static_cast<double>(z), D.invT64, nMTc);
-    int b;
-    double e;
-    if (bf >= 0.0f) {
-      b = static_cast<int>(bf);
-      const double r = fma(static_cast<double>(b), invK, u);
-      const float rf = static_cast<float>(r);
-      const float cf = fmaf(rf, fmaf(rf, 1.0f / 120.0f, 1.0f / 24.0f), 1.0f / 6.0f);
-      double q = fma(static_cast<double>(cf), r, 0.5);
-      q = fma(q, r, 1.0);
-      q = fma(q, r, 1.0);
-      e = sh.u.wtab[b] * q;
-    } else {  // the list above the bins
-      b = -1;
-      e = exp_tang(fmax(u + c0, -700.0), tab);
-    }
-    sT += e;
-    if (b < b_lo) {  // above the window (lanes outside it keep their sums as they are)
-      mA += e;
-      eAu = fma(e, u, eAu);
-    } else if (b <= b_hi) {
-      const uint32_t slot = atomicAdd(&sh.wcount, 1u);
-      if (slot < static_cast<uint32_t>(kCap)) sh.win[slot] = z;
-    }
-  });
-  block_sum2(mA, eAu, sh);
-  const double eA = fma(c0, mA, eAu);
-  double sT2 = sT, unused = 0.0;
-  block_sum2(sT2, unused, sh);
-  const uint32_t cA = above;
-  const uint32_t nw_all = sh.wcount;
-  if (nw_all > static_cast<uint32_t>(kCap)) return false;
-
-  // 3. sort the window (descending), scan its masses, verify the crossing
-  const int nw = static_cast<int>(nw_all);
-  int n2 = 2;
-  while (n2 < nw) n2 <<= 1;
-  for (int i = nw + threadIdx.x; i < n2; i += kTpBlock) sh.win[i] = -INFINITY;
-  __syncthreads();
-  bitonic_desc(sh.win, n2);
-  const int per = (n2 + kTpBlock - 1) / kTpBlock;
-  const int i0 = threadIdx.x * per;
-  const int i1 = i0 + per < nw ? i0 + per : nw;
-  double sm = 0.0, se = 0.0;
-  for (int i = i0; i < i1; ++i) {
-    const double dd = D.d64(sh.win[i]);
-    const double e = exp_tang(dd, tab);
-    sm += e;
-    se += e * dd;
-  }
-  const double cm = block_exclusive_scan(sm, sh);
-  const double ce = block_exclusive_scan(se, sh);
-  double wm = sm, we = se;
-  block_sum2(wm, we, sh);
-  const double S = sT2;  // every binned logit
-  const double target = static_cast<double>(P) * S;
-  if (!(mA < target) || mA + wm < target) return false;  // crossing outside the window
-  if (threadIdx.x == 0) sh.jfirst = 0xffffffffu;
-  __syncthreads();
-  double run_m = mA + cm;
-  for (int i = i0; i < i1; ++i) {
-    run_m += exp_tang(D.d64(sh.win[i]), tab);
-    if (run_m >= target) {
-      atomicMin(&sh.jfirst, static_cast<uint32_t>(i));
-      break;
-    }
-  }
-  __syncthreads();
-  const uint32_t jf = sh.jfirst;
-  if (jf == 0xffffffffu) return false;
-  if (static_cast<int>(jf) >= i0 && static_cast<int>(jf) < i1) {
-    double m2 = mA + cm, e2 = eA + ce;
-    for (int i = i0; i <= static_cast<int>(jf); ++i) {
-      const double dd = D.d64(sh.win[i]);
-      const double e = exp_tang(dd, tab);
-      m2 += e;
-      e2 += e * dd;
-    }
-    sh.SN = m2;
-    sh.EN = e2;
-  }
-  __syncthreads();
-  nuc.k = static_cast<int32_t>(cA + jf + 1);
-  nuc.S = sh.SN;
-  nuc.E = sh.EN;
-  return true;
+  // Sparse pass when few lanes have three buckets reaching the window: a
+  // bucket can reach it only if its maximum does (bf falls with z).
+  auto reaches = [&](float x) { return fmaf(x, hk.kz, hk.k0) < static_cast<float>(W.b_hi + 1); };
+  const bool full = reaches(tk.b3);
+  const int64_t s1 = (tk.b1v >= 0 && reaches(tk.b1)) ? tk.b1v : -1;
+  const int64_t s2 = (tk.b2v >= 0 && reaches(tk.b2)) ? tk.b2v : -1;
+  const uint32_t n_full = block_sum_u(full ? 1u : 0u, sh);
+  if (n_full <= kSparseFullLanes &&
+      exact_cut<Tin, true>(row, V, h, nvec, D, P, hk, sh, W, c0, invK, full, s1, s2, nuc))
+    return true;
+  return exact_cut<Tin, false>(row, V, h, nvec, D, P, hk, sh, W, c0, invK, true, -1, -1, nuc);
 }
 
 }  // namespace
@@ -807,9 +943,12 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
   const bool nucleus_row = Prow > 0.0f && Prow < 1.0f && temperature_ok(cx.T);
   const bool anchored = nucleus_row && A0 > -INFINITY && A0 < INFINITY;
   const float invT = 1.0f / cx.T;
-  HookPair<HistHook, typename std::conditional<SEQ, topk::Hook, NoHook>::type> hp;
+  // The top-K hook keeps each lane's three largest bucket maxima and the
+  // steps of the first two: the sparse exact pass reads those buckets back
+  // (and the sequence variant selects the K largest logits from them).
+  HookPair<HistHook, topk::Hook> hp;
   HistHook& hk = hp.a;
-  if constexpr (SEQ) hp.b.init();
+  hp.b.init();
   hk.bins = sh.u.hs.bins;
   hk.above = sh.above;
   hk.n_above = &sh.n_above;
@@ -872,7 +1011,7 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
   D.invT64 = 1.0 / static_cast<double>(T);
   const float P = Prow;
   Nucleus nuc;
-  if (!(anchored && hist_nucleus<Tin>(row, a.V, cx.h, nvec, D, P, A0, hk, sh, nuc)))
+  if (!(anchored && hist_nucleus<Tin>(row, a.V, cx.h, nvec, D, P, A0, hk, hp.b, sh, nuc)))
     nuc = legacy_nucleus<Tin>(row, a.V, cx.h, nvec, D, P, sh);
   if constexpr (SEQ) {
     if (threadIdx.x < kWave) {

@@ -127,10 +127,9 @@ def test_stored_values_match_generator_and_oracle(fn):
         rows = [0, 1, len(active) - 1]
         P = None
     else:
-        base = name.split("_chunk")[0]
-        w = wl.WORKLOADS[base]
-        if "_chunk" in name:
-            w = wl.offline_chunk(w, int(name.split("_chunk")[1]))
+        w = wl.WORKLOADS[name]
+        if "_chunk" in fn:  # a chunk of whole requests of the offline workload
+            w = wl.offline_chunk(w, int(fn.split("_chunk")[1].split(".")[0]))
         offsets, s, h, j, T, P = wl.batch_plan(w)
         assert np.array_equal(offsets, d["offsets"]) and np.array_equal(T, d["T"])
         n0 = int(offsets[1])
