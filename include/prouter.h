@@ -148,6 +148,25 @@ pr_status pr_token_features(const void* logits, pr_dtype dtype, int64_t n_rows, 
                             const float* top_p, const pr_token_features_t* out, void* workspace,
                             size_t workspace_bytes, void* stream);
 
+/*
+ * pr_token_features for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops or harnesses that forbid
+ * hipMalloc): the same arguments and outputs without the workspace. The
+ * split-row scratch that small batches need (fewer than 256 rows) lives in a
+ * static device array of PR_NOALLOC_SCRATCH_BYTES that each GPU holds until
+ * the process ends; its address is looked up on the first call on a device.
+ * Nothing is allocated and nothing needs clearing (every scratch entry is
+ * written before it is read in the same call). Calls that overlap on one GPU
+ * (other streams or host threads) share the array and race: serialise them.
+ * Returns PR_ERR_UNSUPPORTED when a shape would need more scratch than the
+ * array holds (no accepted shape does: the most is 12,272 bytes, 256 rows' or
+ * workgroups' partial states), PR_ERR_HIP when the address lookup fails.
+ */
+#define PR_NOALLOC_SCRATCH_BYTES 16384
+pr_status pr_token_features_noalloc(const void* logits, pr_dtype dtype, int64_t n_rows, int32_t vocab,
+                                    int64_t row_stride, const int32_t* sampled_ids, const float* temperature,
+                                    const float* top_p, const pr_token_features_t* out, void* stream);
+
 /* Largest K of pr_feature_sequence's top-K entropy. */
 #define PR_MAX_TOP_K 32
 

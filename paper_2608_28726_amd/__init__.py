@@ -25,7 +25,7 @@ from . import _abi
 from ._abi import (FLAG_BAD_ID, FLAG_BAD_TP, FLAG_NONFINITE, FLAG_OUTSIDE_NUCLEUS,  # noqa: F401
                    ProuterError)
 
-__all__ = ["token_features", "feature_sequence", "sample_features", "verifier_head", "request_aggregate", "route", "calibrate_threshold",
+__all__ = ["token_features", "token_features_noalloc", "feature_sequence", "sample_features", "verifier_head", "request_aggregate", "route", "calibrate_threshold",
            "validate_offsets", "StreamState",
            "token_features_workspace", "ProuterError", "FEATURE_FLOATS", "FEATURE_INTS", "PAPER_TOP_K"]
 
@@ -138,6 +138,27 @@ def token_features(logits: torch.Tensor, sampled_ids: torch.Tensor, temperature,
                              _ptr(top_p), C.byref(_features_struct(out)), _ptr(workspace), ws_bytes,
                              _stream_handle())
     _abi.check("pr_token_features", st)
+    return out
+
+
+def token_features_noalloc(logits: torch.Tensor, sampled_ids: torch.Tensor, temperature, top_p=None,
+                           out: dict | None = None) -> dict:
+    """``pr_token_features_noalloc``: :func:`token_features` with the library's
+    static per-GPU scratch instead of a workspace (nothing is allocated by the
+    library; pass ``out`` to allocate nothing here either). Calls that overlap
+    on one GPU race on that scratch."""
+    n, V = logits.shape
+    temperature = _as_row_tensor(temperature, n, logits.device)
+    top_p = None if top_p is None else _as_row_tensor(top_p, n, logits.device)
+    _check_rows(logits, sampled_ids, temperature, top_p)
+    if out is None:
+        out = _alloc_features(n, logits.device)
+    else:
+        _check_features(out, logits.device, n, "out")
+    st = _abi.lib().pr_token_features_noalloc(_ptr(logits), _dtype_code(logits), n, V, logits.stride(0),
+                                              _ptr(sampled_ids), _ptr(temperature), _ptr(top_p),
+                                              C.byref(_features_struct(out)), _stream_handle())
+    _abi.check("pr_token_features_noalloc", st)
     return out
 
 

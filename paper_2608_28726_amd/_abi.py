@@ -24,7 +24,7 @@ EXPORTED = (
     "pr_request_aggregate", "pr_route", "pr_validate_offsets", "pr_stream_create", "pr_stream_step",
     "pr_stream_finish", "pr_stream_reset_slots", "pr_stream_destroy", "pr_feature_sequence",
     "pr_verifier_head_workspace", "pr_verifier_head", "pr_calibrate_threshold",
-    "pr_calibrate_workspace", "pr_sample_features",
+    "pr_calibrate_workspace", "pr_sample_features", "pr_token_features_noalloc",
 )
 
 PR_HEAD_WEIGHTS = 67329
@@ -72,6 +72,8 @@ def lib() -> C.CDLL:
     L.pr_token_features_workspace.restype = sz
     L.pr_token_features.argtypes = [vp, C.c_int, i64, i32, i64, vp, vp, vp, C.POINTER(TokenFeatures), vp, sz, vp]
     L.pr_token_features.restype = C.c_int
+    L.pr_token_features_noalloc.argtypes = [vp, C.c_int, i64, i32, i64, vp, vp, vp, C.POINTER(TokenFeatures), vp]
+    L.pr_token_features_noalloc.restype = C.c_int
     L.pr_feature_sequence.argtypes = [vp, C.c_int, i64, i32, i64, vp, vp, vp, vp, i32, i32, vp,
                                       C.POINTER(TokenFeatures), vp]
     L.pr_feature_sequence.restype = C.c_int

@@ -1,6 +1,7 @@
 // C ABI of the verifier library: argument checks, launch-shape selection and
 // the streaming state object. Every compute step runs in the kernels of
 // row_features.hip, topp.hip and aggregate.hip.
+#include <mutex>
 #include <new>
 
 #include "aggregate.h"
@@ -9,6 +10,13 @@
 #include "topp.h"
 
 using namespace pr;
+
+// Scratch of pr_token_features_noalloc: the split-row partial states of small
+// batches, in a file-scope device array instead of a caller's workspace. Each
+// GPU the library runs on holds its own copy until the process ends. In host
+// code this name is only a stand-in for the symbol: its device address comes
+// from hipGetSymbolAddress (see noalloc_scratch below), never from the name.
+static __device__ __align__(256) unsigned char scratch[PR_NOALLOC_SCRATCH_BYTES];
 
 struct pr_stream {
   int device;
@@ -61,6 +69,36 @@ pr_agg_params default_params() {
   p.b = 0.0;
   p.link = 0;
   return p;
+}
+
+// Device address of `scratch` on the device that runs `stream` (the current
+// device for the NULL stream), looked up once per device with that device
+// current and kept. No allocation happens here or later.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+pr_status noalloc_scratch(hipStream_t stream, void** out) {
+  int cur = 0;
+  if (hipGetDevice(&cur) != hipSuccess) return PR_ERR_HIP;
+  int dev = cur;
+  if (stream) {
+    hipDevice_t d = 0;
+    if (hipStreamGetDevice(stream, &d) != hipSuccess) return PR_ERR_HIP;
+    dev = static_cast<int>(d);
+  }
+  if (dev < 0 || dev >= kMaxDevices) return PR_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    if (dev != cur && hipSetDevice(dev) != hipSuccess) return PR_ERR_HIP;
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur && hipSetDevice(cur) != hipSuccess) return PR_ERR_HIP;
+    if (e != hipSuccess || !p) return PR_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return PR_OK;
 }
 
 bool params_ok(const pr_agg_params& p) {
@@ -123,6 +161,24 @@ pr_status pr_token_features(const void* logits, pr_dtype dtype, int64_t n_rows, 
   a.G = row_split(n_rows, vocab, dtype);
   a.ws = static_cast<Partial*>(workspace);
   return hip_status(launch_row_features(a, dtype, as_stream(stream)));
+}
+
+pr_status pr_token_features_noalloc(const void* logits, pr_dtype dtype, int64_t n_rows, int32_t vocab,
+                                    int64_t row_stride, const int32_t* sampled_ids, const float* temperature,
+                                    const float* top_p, const pr_token_features_t* out, void* stream) {
+  pr_status st = check_rows(logits, dtype, n_rows, vocab, row_stride, sampled_ids, temperature);
+  if (st != PR_OK) return st;
+  if (!features_complete(out)) return PR_ERR_INVALID_ARG;
+  const size_t need = pr_token_features_workspace(dtype, n_rows, vocab, top_p ? 1 : 0);
+  if (need > PR_NOALLOC_SCRATCH_BYTES) return PR_ERR_UNSUPPORTED;
+  if (n_rows == 0) return PR_OK;
+  void* ws = nullptr;
+  if (need > 0) {
+    st = noalloc_scratch(as_stream(stream), &ws);
+    if (st != PR_OK) return st;
+  }
+  return pr_token_features(logits, dtype, n_rows, vocab, row_stride, sampled_ids, temperature, top_p, out, ws,
+                           need, stream);
 }
 
 pr_status pr_feature_sequence(const void* logits, pr_dtype dtype, int64_t n_rows, int32_t vocab,
