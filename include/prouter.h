@@ -30,7 +30,16 @@
 extern "C" {
 #endif
 
-typedef enum pr_status {
+/* The enumerations are int-sized in C. C++ gives them int as a fixed
+ * underlying type, so that a caller's out-of-range value (which the calls
+ * reject) is still a valid value of the type there. */
+#ifdef __cplusplus
+#define PR_ENUM_BASE : int
+#else
+#define PR_ENUM_BASE
+#endif
+
+typedef enum pr_status PR_ENUM_BASE {
   PR_OK = 0,
   PR_ERR_INVALID_ARG = 1,
   PR_ERR_UNSUPPORTED = 2,
@@ -39,7 +48,7 @@ typedef enum pr_status {
 } pr_status;
 
 /* Storage type of the logits. bf16 is the upper 16 bits of an IEEE float32. */
-typedef enum pr_dtype { PR_F32 = 0, PR_BF16 = 1 } pr_dtype;
+typedef enum pr_dtype PR_ENUM_BASE { PR_F32 = 0, PR_BF16 = 1 } pr_dtype;
 
 /* Per-row flags (bit set in pr_token_features_t.flags). */
 #define PR_FLAG_NONFINITE 1u       /* a NaN or +inf logit, or every logit is -inf; all float

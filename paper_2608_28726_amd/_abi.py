@@ -5,7 +5,9 @@ from __future__ import annotations
 import ctypes as C
 import os
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libprouter.so")
+# The library next to this file; PR_LIBRARY names another build of it (the
+# host-sanitized build, see build.py).
+LIB_PATH = os.environ.get("PR_LIBRARY") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libprouter.so")
 
 PR_OK, PR_ERR_INVALID_ARG, PR_ERR_UNSUPPORTED, PR_ERR_HIP, PR_ERR_NO_MEMORY = range(5)
 PR_F32, PR_BF16 = 0, 1

@@ -59,13 +59,22 @@ def compare_rows(f: dict, g: dict, what: str, sel=slice(None)):
 
 
 def compare_requests(a: dict, g: dict, prefix: str, tau: float, what: str):
-    """Per-request count, summaries, score and decision against stored ones."""
+    """Per-request count, summaries, score and decision against stored ones.
+    Besides the workload's threshold, the decisions are also compared at the
+    median of the oracle's scores, where about half the requests ship."""
     assert_ints(f"{what} count", a["count"], g[prefix + "count"])
     for stat in ("mean", "min", "quant"):
         assert_floats(f"{what} {stat}", a[stat], g[prefix + stat])
     assert_floats(f"{what} score", a["score"], g[prefix + "score"])
     ok = decisions_agree(a["ship"], g[prefix + "score"], tau)
     assert ok.all(), f"{what}: decisions differ for requests {np.flatnonzero(~ok).tolist()}"
+    tau_med = float(np.float32(np.nanmedian(g[prefix + "score"])))
+    ship_med, n_med = pr.route(torch.as_tensor(np.asarray(a["score"], dtype=np.float32)).cuda(), tau_med)
+    ship_med = ship_med.cpu().numpy()
+    ok = decisions_agree(ship_med, g[prefix + "score"], tau_med)
+    assert ok.all(), f"{what}: decisions at the median differ for requests {np.flatnonzero(~ok).tolist()}"
+    print(f"  {what}: {int(a['ship'].sum())} of {len(ok)} ship at tau = {tau}, {int(ship_med.sum())} at the "
+          f"median score {tau_med:.6f}", flush=True)
 
 
 def device_batch(w, g):
