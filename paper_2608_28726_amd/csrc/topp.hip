@@ -758,9 +758,14 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   // are not unrolled (one copy of the float64 exp each; the second loop
   // recomputes the masses of the first), and the crossing bins are found
   // with a ballot and one LDS atomic per wave.
-  auto centre_mass = [&](int b) -> double { return exp(fma(-(static_cast<double>(b) + 0.5), hb, lead)); };
-  auto bin_mass = [&](int b) -> double {
-    const double w = centre_mass(b);
+  // A thread's kPer consecutive bins: centre masses by the recurrence
+  // w_{b+1} = w_b * exp(-hb) from one exp per thread (kPer - 1 roundings,
+  // below 1e-15 relative).
+  constexpr int kPer = kHB / kTpBlock;
+  const int b0 = threadIdx.x * kPer;
+  const double w0 = exp(fma(-(static_cast<double>(b0) + 0.5), hb, lead));
+  const double rho = exp(-hb);
+  auto bin_mass = [&](int b, double w) -> double {
     const uint64_t word = sh.u.hs.bins[b];
     const double cnt = static_cast<double>(static_cast<uint32_t>(word >> kCountShift));
     const double dsum =
@@ -769,11 +774,12 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   };
   double sa = 0.0;
   for (uint32_t i = threadIdx.x; i < n_above; i += kTpBlock) sa += exp_tang(D.d64(sh.above[i]), tab);
-  constexpr int kPer = kHB / kTpBlock;
-  const int b0 = threadIdx.x * kPer;
   double seg = 0.0;
+  {
+    double w = w0;
 #pragma unroll 1
-  for (int k = 0; k < kPer; ++k) seg += bin_mass(b0 + k);
+    for (int k = 0; k < kPer; ++k, w *= rho) seg += bin_mass(b0 + k, w);
+  }
   double tot = seg;
   block_sum2(sa, tot, sh);
   tot += sa;
@@ -789,9 +795,10 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
     // this thread's first bins where the running mass reaches t_lo and t_hi
     int k_lo = kHB, k_hi = kHB;
     double c = before;
+    double w = w0;
 #pragma unroll 1
-    for (int k = 0; k < kPer; ++k) {
-      c += bin_mass(b0 + k);
+    for (int k = 0; k < kPer; ++k, w *= rho) {
+      c += bin_mass(b0 + k, w);
       if (k_lo == kHB && c >= t_lo) k_lo = b0 + k;
       if (k_hi == kHB && c >= t_hi) k_hi = b0 + k;
     }
@@ -812,17 +819,20 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   W.b_hi = sa >= t_hi ? -1 : sh.hb_hi;
   uint32_t inwin = 0, above = 0;
   double sb = 0.0, sb_max = 0.0;
+  {
+    double w = w0;
 #pragma unroll 1
-  for (int k = 0; k < kPer; ++k) {
-    const int b = b0 + k;
-    const uint32_t cnt = static_cast<uint32_t>(sh.u.hs.bins[b] >> kCountShift);
-    if (b < W.b_lo) {
-      above += cnt;
-    } else if (b <= W.b_hi) {
-      inwin += cnt;
-    } else if (cnt) {  // below the window: the estimate and a bound on its error
-      sb += bin_mass(b);
-      sb_max += static_cast<double>(cnt) * centre_mass(b);
+    for (int k = 0; k < kPer; ++k, w *= rho) {
+      const int b = b0 + k;
+      const uint32_t cnt = static_cast<uint32_t>(sh.u.hs.bins[b] >> kCountShift);
+      if (b < W.b_lo) {
+        above += cnt;
+      } else if (b <= W.b_hi) {
+        inwin += cnt;
+      } else if (cnt) {  // below the window: the estimate and a bound on its error
+        sb += bin_mass(b, w);
+        sb_max += static_cast<double>(cnt) * w;
+      }
     }
   }
   W.inwin = block_sum_u(inwin, sh) + (W.b_lo < 0 ? n_above : 0u);
@@ -840,8 +850,12 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   // takes the table-driven exp.
   const double lead0 = (static_cast<double>(A0) - static_cast<double>(D.M)) * D.invT64 + kHAbove;
   const double c0 = lead0 - 0.5 * invK;  // centre of bin b: c0 - b * invK
+  {
+    double w = exp(fma(-static_cast<double>(b0), invK, c0));
+    const double rk = exp(-invK);
 #pragma unroll 1
-  for (int k = 0; k < kPer; ++k) sh.u.wtab[b0 + k] = exp(fma(-static_cast<double>(b0 + k), invK, c0));
+    for (int k = 0; k < kPer; ++k, w *= rk) sh.u.wtab[b0 + k] = w;
+  }
   __syncthreads();
 
   // Sparse pass when few lanes have three buckets reaching the window: a
