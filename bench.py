@@ -162,7 +162,8 @@ def cpu_baseline(torch, batch, gpu_out, seconds, mode="features", top_k=20, skip
         _oracle_init(tmp, dtype, mode, top_k)
         res = []
         t0 = time.perf_counter()
-        while len(res) < min(n_max, 8) or (len(res) < n_max and time.perf_counter() - t0 < 0.3 * seconds):
+        n1_cap = max(8, n_max // 4)  # leave rows for the all-core run on small batches
+        while len(res) < min(n_max, 8) or (len(res) < n1_cap and time.perf_counter() - t0 < 0.3 * seconds):
             res += _oracle_rows([len(res)])
         t1 = time.perf_counter() - t0
         n1 = len(res)
@@ -497,6 +498,12 @@ def run_stream(args, torch, pr, wl, w):
     if not (eager_ok and replays_ok):
         raise RuntimeError("streaming verdicts of the graph replays differ from the eager pass")
 
+    # The oracle baseline takes the first pool step's rows (one full step of
+    # 256 rows), with their features from the same row kernel tier.
+    logits0, ids0, T0 = pool[0]
+    feats0 = pr.token_features(logits0, ids0, T0)
+    torch.cuda.synchronize()
+    batch0 = wl.Batch(w, np.array([0, w.n_req], dtype=np.int32), logits0, ids0, T0, None)
     bytes_step = w.n_req * algorithmic_bytes_per_row(w.V, w.elem_bytes)
     extra = {"kernel": "row_features_kernel (streaming step, 256 rows)", "kernel_ms": kern_full,
              "timing": f"kernel_ms: HIP events around {5 * n_full} back-to-back full 256-row steps replayed "
@@ -511,7 +518,7 @@ def run_stream(args, torch, pr, wl, w):
     log(f"[bench] stream: {n_steps} steps, {rows} rows; graph pass {pass_ms:.3f} ms "
         f"({pass_ms * 1e3 / n_steps:.1f} us/step), full-step row kernel {kern_full * 1e3:.1f} us; "
         f"eager (host-paced) p50 {extra['eager_step_us_p50']:.1f} us, wall {extra['eager_wall_us_per_step']:.1f} us/step")
-    return None, None, rows, pass_ms * 1e-3, kern_full, bytes_step, extra
+    return batch0, feats0, rows, pass_ms * 1e-3, kern_full, bytes_step, extra
 
 
 def run_calibrate(args, torch, pr, wl):
