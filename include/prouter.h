@@ -368,7 +368,9 @@ pr_status pr_stream_create(int32_t max_slots, int32_t max_len, const pr_agg_para
  * Tokens past max_len are counted in sums and minima but not kept, and the
  * slot's quantile becomes NaN. In bounded-memory mode (max_len == 0) the
  * token instead updates the slot's P-square markers. out may be NULL (features not returned).
- * top_p must be NULL (PR_ERR_UNSUPPORTED otherwise).
+ * top_p (device float [n_active]) or NULL: with it, the features and the
+ * tuple A that joins the slot are those of the renormalised nucleus, as in
+ * pr_token_features (vocab below 2^24, PR_ERR_UNSUPPORTED otherwise).
  */
 pr_status pr_stream_step(pr_stream* state, const void* logits, pr_dtype dtype, int32_t n_active,
                          int32_t vocab, int64_t row_stride, const int32_t* slot_ids,

@@ -361,10 +361,12 @@ class StreamState:
                                                                      C.byref(self._h)))
         self.max_slots, self.max_len = max_slots, max_len
 
-    def step(self, logits, slot_ids, sampled_ids, temperature, out: dict | None = None, want_features=False):
+    def step(self, logits, slot_ids, sampled_ids, temperature, out: dict | None = None, want_features=False,
+             top_p=None):
         n, V = logits.shape
         temperature = _as_row_tensor(temperature, n, logits.device)
-        _check_rows(logits, sampled_ids, temperature, None)
+        top_p = None if top_p is None else _as_row_tensor(top_p, n, logits.device)
+        _check_rows(logits, sampled_ids, temperature, top_p)
         _check_index_tensor(slot_ids, "slot_ids", logits.device, n)
         if out is None and want_features:
             out = _alloc_features(n, logits.device)
@@ -372,7 +374,7 @@ class StreamState:
             _check_features(out, logits.device, n, "out")
         fs = C.byref(_features_struct(out)) if out is not None else None
         st = _abi.lib().pr_stream_step(self._h, _ptr(logits), _dtype_code(logits), n, V, logits.stride(0),
-                                       _ptr(slot_ids), _ptr(sampled_ids), _ptr(temperature), None, fs,
+                                       _ptr(slot_ids), _ptr(sampled_ids), _ptr(temperature), _ptr(top_p), fs,
                                        _stream_handle())
         _abi.check("pr_stream_step", st)
         return out

@@ -383,7 +383,7 @@ pr_status pr_stream_step(pr_stream* state, const void* logits, pr_dtype dtype, i
   if (st != PR_OK) return st;
   if (n_active > state->dev.max_slots) return PR_ERR_INVALID_ARG;
   if (n_active > 0 && !slot_ids) return PR_ERR_INVALID_ARG;
-  if (top_p) return PR_ERR_UNSUPPORTED;
+  if (top_p && vocab >= kTopPMaxVocab) return PR_ERR_UNSUPPORTED;
   if (out && !features_complete(out)) return PR_ERR_INVALID_ARG;
   if (n_active == 0) return PR_OK;
   RowArgs a{};
@@ -393,7 +393,7 @@ pr_status pr_stream_step(pr_stream* state, const void* logits, pr_dtype dtype, i
   a.row_stride = row_stride;
   a.sampled_ids = sampled_ids;
   a.temperature = temperature;
-  a.top_p = nullptr;
+  a.top_p = top_p;
   if (out) a.out = *out;
   int G = row_split(n_active, vocab, dtype);
   if (G > kStreamMaxSplit) G = kStreamMaxSplit;
@@ -401,6 +401,7 @@ pr_status pr_stream_step(pr_stream* state, const void* logits, pr_dtype dtype, i
   a.ws = state->ws;
   a.slot_ids = slot_ids;
   a.st = state->dev;
+  if (top_p) return hip_status(launch_topp(a, dtype, nullptr, as_stream(stream)));
   return hip_status(launch_row_features(a, dtype, as_stream(stream)));
 }
 

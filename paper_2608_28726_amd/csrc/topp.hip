@@ -37,6 +37,7 @@
 
 #include <type_traits>
 
+#include "p2.h"
 #include "row_scan.h"
 #include "topk.h"
 
@@ -915,6 +916,22 @@ __device__ __forceinline__ topk::Lds topk_lds(TpShared& sh) {
   return s;
 }
 
+// Finalises row r (wave 0 of the workgroup): its features and, in a
+// streaming step (slot ids given), the token's join to its request slot:
+// count, sums, minima and history, or the P-square markers.
+__device__ __forceinline__ void finish_row(const RowArgs& a, int64_t r, const Partial& p, const RowCtx& cx,
+                                           uint32_t fix, const Nucleus* nuc) {
+  if (threadIdx.x >= kWave) return;
+  p2::RowMarkers pm;
+  pm.fetch(a, r);
+  float conf[4];
+  if (threadIdx.x == 0) {
+    finalize_row(a, r, p, cx, fix, conf, nuc);
+    stream_update(a.st, slot_load(a, r), conf);
+  }
+  if (pm.slot >= 0) p2::feed_row(a, pm, conf);
+}
+
 // SEQ: also the row's K largest logits (found in the stats pass) and row r
 // of the verifier input sequence X, with the top-K probabilities taken on the
 // renormalised nucleus.
@@ -1011,10 +1028,7 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
       }
       return;
     }
-    if (threadIdx.x == 0) {
-      float conf[4];
-      finalize_row(a, r, p, cx, fix, conf);
-    }
+    finish_row(a, r, p, cx, fix, nullptr);
     return;
   }
 
@@ -1040,10 +1054,7 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
     }
     return;
   }
-  if (threadIdx.x == 0) {
-    float conf[4];
-    finalize_row(a, r, p, cx, fix, conf, &nuc);
-  }
+  finish_row(a, r, p, cx, fix, &nuc);
 }
 
 size_t topp_workspace(pr_dtype, int64_t, int32_t) { return 0; }

@@ -97,3 +97,79 @@ def test_stream_overflow_and_reset():
     torch.cuda.synchronize()
     assert (res2["count"].cpu().numpy() == 0).all()
     st.close()
+
+
+def _stream_over_batch(b, max_len, q):
+    """Feeds a host-made batch to a stream, request i in slot i, one token per
+    step; returns each step's features and every slot's finish result."""
+    lengths = np.diff(b.offsets)
+    logits, ids, T, P = (t.cuda() for t in (b.logits, b.sampled_ids, b.temperature, b.top_p))
+    st = pr.StreamState(len(lengths), max_len, q=q)
+    steps = []
+    results = {}
+    for t in range(int(lengths.max())):
+        active = np.flatnonzero(lengths > t).astype(np.int32)
+        rows = torch.as_tensor(b.offsets[active] + t, dtype=torch.int64).cuda()
+        out = st.step(logits[rows].contiguous(), torch.as_tensor(active).cuda(), ids[rows].contiguous(),
+                      T[rows].contiguous(), want_features=True, top_p=P[rows].contiguous())
+        torch.cuda.synchronize()
+        steps.append((rows.cpu().numpy(), {k: v.cpu().numpy() for k, v in out.items()}))
+        ending = active[lengths[active] == t + 1]
+        if len(ending):
+            res = st.finish(torch.as_tensor(ending).cuda(), 0.5)
+            torch.cuda.synchronize()
+            for k, s in enumerate(ending):
+                results[int(s)] = {key: v[k].cpu().numpy() for key, v in res.items()}
+    st.close()
+    return steps, results
+
+
+@pytest.mark.parametrize("V,dtype", [(4096, "f32"), (151936, "bf16")])
+def test_stream_with_top_p_matches_offline_and_oracle(V, dtype):
+    """Streaming steps with top-p: every step's features equal the oracle's on
+    the renormalised nucleus, and each request's verdict at its finish equals
+    the offline path's and the oracle's over the same rows."""
+    w = wl.scaled(wl.WORKLOADS["topp_128x256_v262144_f32"], n_req=7, len_lo=2, len_hi=9, V=V, dtype=dtype,
+                  seed=0x5053)
+    b = wl.make_batch(w, device="cpu")
+    print(f"case stream top-p V={V} {dtype} rows={b.n_rows}", flush=True)
+    steps, results = _stream_over_batch(b, 16, w.q)
+    o = oracle_features(b.logits.cuda(), b.sampled_ids.cuda(), b.temperature.cuda(), b.top_p.cuda())
+    for k, (rows, f) in enumerate(steps):
+        compare_features(f, {key: v[rows] for key, v in o.items()}, what=f"step {k + 1} ")
+    oa = oagg.request_aggregate(o, b.offsets, q=w.q)
+    os_ = oagg.score_from_aggregates(oa)
+    feats = pr.token_features(b.logits.cuda(), b.sampled_ids.cuda(), b.temperature.cuda(), b.top_p.cuda())
+    agg = pr.request_aggregate(feats, torch.as_tensor(b.offsets).cuda(), q=w.q)
+    torch.cuda.synchronize()
+    for i in range(w.n_req):
+        r = results[i]
+        assert int(r["count"]) == b.offsets[i + 1] - b.offsets[i]
+        for stat in ("min", "quant"):  # streaming == offline exactly for selections
+            a_, g_ = r[stat].astype(np.float64), agg[stat][i].cpu().numpy().astype(np.float64)
+            assert ((a_ == g_) | (np.isnan(a_) & np.isnan(g_))).all(), (i, stat, a_, g_)
+        for stat in ("mean", "min", "quant"):
+            assert_floats(f"req {i} {stat} vs oracle", r[stat], oa[stat][i])
+        assert_floats(f"req {i} score vs oracle", np.array([r["score"]]), np.array([os_[i]]))
+        assert decisions_agree(np.array([r["ship"]]), np.array([os_[i]]), 0.5).all()
+
+
+def test_stream_with_top_p_bounded_memory():
+    """The P-square quantile of a streaming run with top-p equals the oracle's
+    P-square estimate over the same per-token tuples."""
+    import oracle
+    w = wl.scaled(wl.WORKLOADS["topp_128x256_v262144_f32"], n_req=4, len_lo=3, len_hi=12, V=2048, seed=0x5054)
+    b = wl.make_batch(w, device="cpu")
+    steps, results = _stream_over_batch(b, 0, 0.3)
+    lengths = np.diff(b.offsets)
+    A = {i: [] for i in range(w.n_req)}
+    for rows, f in steps:
+        for k, row in enumerate(rows):
+            i = int(np.searchsorted(b.offsets, row, side="right") - 1)
+            A[i].append((f["logprob"][k], f["maxprob"][k], -f["entropy"][k], f["margin"][k]))
+    for i in range(w.n_req):
+        assert len(A[i]) == lengths[i]
+        for c in range(4):
+            e = np.float32(oracle.p2_quantile([np.float32(a[c]) for a in A[i]], 0.3))
+            got = results[i]["quant"][c]
+            assert got == e or (np.isnan(e) and np.isnan(got)), (i, c, got, e)
