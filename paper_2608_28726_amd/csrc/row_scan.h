@@ -221,7 +221,7 @@ __device__ __forceinline__ void consume_scalar(float z, int64_t idx, const RowCt
 // publishes it; after one barrier the first wave merges the NW wave states
 // with lane-parallel reductions.
 template <int BLOCK>
-__device__ Partial block_merge(Lane& L, float c) {
+__device__ __forceinline__ Partial block_merge(Lane& L, float c) {
   constexpr int NW = BLOCK / kWave;
   static_assert(NW >= 1 && NW <= kWave, "one wave merges the wave states");
   __shared__ Partial sh[NW];
@@ -279,7 +279,7 @@ __device__ __forceinline__ int64_t head_elems(const void* row, int32_t V) {
 }
 
 template <typename Tin>
-__device__ RowCtx row_ctx(const RowArgs& a, int64_t r, const void* row) {
+__device__ __forceinline__ RowCtx row_ctx(const RowArgs& a, int64_t r, const void* row) {
   constexpr int VEC = Elem<Tin>::kVec;
   RowCtx cx;
   const float T = a.temperature[r];
@@ -483,7 +483,7 @@ __device__ void scan_stretch(const void* row, int32_t V, int64_t vb, int64_t ve,
 // summed over the block. z_y is the same in every thread, so the barrier
 // below is reached by all threads or by none.
 template <typename Tin, int BLOCK>
-__device__ uint32_t rank_fixup(const void* row, int32_t V, int64_t nvec, const RowCtx& cx) {
+__device__ __forceinline__ uint32_t rank_fixup(const void* row, int32_t V, int64_t nvec, const RowCtx& cx) {
   constexpr int VEC = Elem<Tin>::kVec;
   if (cx.y < 0) return 0;
   if (cx.zy != -INFINITY) return cx.fix_vec;

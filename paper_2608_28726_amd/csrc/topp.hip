@@ -278,7 +278,7 @@ __device__ void bitonic_desc(float* a, int n2) {
 // are float atomics and only choose the digits; the masses that reach the
 // result are summed again in a fixed order once the boundary value is known.
 template <typename Tin>
-__device__ Nucleus radix_boundary(const void* row, int32_t V, int64_t h, int64_t nvec, const Dist& D, TpShared& sh) {
+__device__ Nucleus radix_boundary(const void* row, int32_t V, int64_t h, int64_t nvec, const Dist D, TpShared& sh) {
   const double massAbove0 = sh.massAbove, Eabove0 = sh.Eabove;
   const uint32_t blo = sh.b_lo, bhi = sh.b_hi;
   double massGT = massAbove0, EGT = Eabove0;
@@ -367,7 +367,7 @@ __device__ Nucleus radix_boundary(const void* row, int32_t V, int64_t h, int64_t
 // exact sums above the crossing bins with their logits gathered, sorted and
 // scanned; radix refinement when the crossing bins are overfull).
 template <typename Tin>
-__device__ Nucleus legacy_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec, const Dist& D, float P,
+__device__ Nucleus legacy_nucleus(const void* row, int32_t V, int64_t h, int64_t nvec, const Dist D, float P,
                                   TpShared& sh) {
   // histogram of the candidates' masses over distance bins
   __syncthreads();
