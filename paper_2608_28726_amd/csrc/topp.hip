@@ -58,7 +58,8 @@ constexpr float kHSpan = 75.0f;   // nats covered: [-kHAbove, kDMax)
 constexpr float kHK = kHB / kHSpan;  // bins per nat
 constexpr int kAboveCap = 512;    // logits above the bins, kept in a list
 constexpr double kWinMargin = 5e-4;  // relative margin of the window around P * S
-constexpr float kOffQ = 4096.0f;     // fixed-point scale of the offsets from the bin centre
+constexpr int kOffBits = 12;         // fixed-point bits of a logit's position inside its bin
+constexpr float kOffQ = 4096.0f;     // 2^kOffBits
 constexpr int kCountShift = 40;      // a histogram word: count << kCountShift | offset sum
 
 struct TpShared {
@@ -68,11 +69,11 @@ struct TpShared {
       uint32_t cnt[kBins];
     } lg;              // fallback histogram
     struct {
-      // stats-pass histogram (+ one discard slot per lane): per bin, the
-      // count (top 24 bits) and the summed offsets from the bin centre
-      // (low 40 bits: each logit adds round((offset + 1/2) * kOffQ) in
-      // [0, kOffQ], so the field stays below 2^40 while V < 2^24)
-      uint64_t bins[kHB + kWave];
+      // stats-pass histogram: per bin, the count (top 24 bits) and the
+      // summed positions inside the bin (low 40 bits: each logit adds
+      // floor((offset + 1/2) * kOffQ) in [0, kOffQ), so the field stays
+      // below 2^40 while V < 2^24)
+      uint64_t bins[kHB];
     } hs;
     double wtab[kHB];  // exact pass: exp of each bin centre's distance from M
   } u;
@@ -207,35 +208,33 @@ __device__ __forceinline__ double exp_tang(double d, const double* tab) {
   return tab[ni & 63] * p * scale;
 }
 
-// Stats-pass histogram: logit z counts in bin floor(bf), bf = fma(z, kz, k0)
-// = (A0 - z) / T * kHK + kHAbove * kHK, and adds its offset bf - floor(bf) -
-// 1/2 from the centre (both in one 64-bit word); bf < 0 (more than kHAbove nats above A0) goes to the
-// list instead, bf >= kHB is beyond the window. Lanes with no bin update a
-// discard slot of their own (kHB + lane), so the update is branch-free and
-// discards do not collide. The exact pass recomputes bf with the same
-// operands, so both passes bin identically.
+// Stats-pass histogram. A logit's bin coordinate is bf = (A0 - z) / T * kHK
+// + kHAbove * kHK; it is formed scaled by kOffQ, x = fma(z, kz4, k04) with
+// kz4 = kOffQ kz and k04 = kOffQ k0 (a power of two: x = kOffQ fma(z, kz, k0)
+// exactly), so that one conversion gives the bin floor(bf) (the high bits of
+// floor(x)) and the logit's position inside it (the low kOffBits bits:
+// floor((bf - floor(bf)) kOffQ)). Both go to the bin in one 64-bit atomic;
+// x < 0 (more than kHAbove nats above A0) goes to the list instead, bf >=
+// kHB is beyond the window (no update). The exact pass recomputes x with
+// the same operands, so both passes bin identically.
 struct HistHook {
   uint64_t* bins;
   float* above;
   uint32_t* n_above;
-  float kz, k0;     // bin coordinate
-  int32_t discard;  // this lane's discard slot
+  float kz, k0;    // bin coordinate bf = fma(z, kz, k0)
+  float kz4, k04;  // the same scaled by kOffQ
   __device__ __forceinline__ void count(float z) {
-    const float bf = fmaf(z, kz, k0);
-    const bool in = bf >= 0.0f && bf < static_cast<float>(kHB);
-    const float bc = fminf(fmaxf(bf, 0.0f), static_cast<float>(kHB));  // NaN -> 0
-    const int b = static_cast<int>(bc);
-    const int idx = in ? b : discard;
-    // one 64-bit atomic: count and the offset from the centre rounded to the
-    // nearest 1/kOffQ, biased by 1/2: bc - floor(bc) in [0, 1) for a counted logit
-    const uint32_t q = static_cast<uint32_t>(fmaf(__builtin_amdgcn_fractf(bc), kOffQ, 0.5f));
-    atomicAdd(&bins[idx], (uint64_t{1} << kCountShift) | q);
+    const float x = fmaf(z, kz4, k04);
+    if (x >= 0.0f && x < static_cast<float>(kHB) * kOffQ) {
+      const uint32_t xi = static_cast<uint32_t>(x);
+      atomicAdd(&bins[xi >> kOffBits], (uint64_t{1} << kCountShift) | (xi & ((1u << kOffBits) - 1)));
+    }
   }
   template <int N>
   __device__ __forceinline__ void step(const float (&z)[N], const float (&)[N], float cmax, int64_t, const Lane&) {
 #pragma unroll
     for (int k = 0; k < N; ++k) count(z[k]);
-    if (__any(fmaf(cmax, kz, k0) < 0.0f)) {  // bf is non-increasing in z
+    if (__any(fmaf(cmax, kz4, k04) < 0.0f)) {  // x is non-increasing in z
 #pragma unroll
       for (int k = 0; k < N; ++k) add_above(z[k]);
     }
@@ -246,7 +245,7 @@ struct HistHook {
   }
   __device__ __forceinline__ void finish(const Lane&) {}
   __device__ __forceinline__ void add_above(float z) {
-    if (fmaf(z, kz, k0) < 0.0f) {
+    if (fmaf(z, kz4, k04) < 0.0f) {
       const uint32_t slot = atomicAdd(n_above, 1u);
       if (slot < static_cast<uint32_t>(kAboveCap)) above[slot] = z;
     }
@@ -612,18 +611,14 @@ __device__ bool exact_cut(const void* row, int32_t V, int64_t h, int64_t nvec, c
   uint32_t nA = 0;
   const double nMTc = -static_cast<double>(D.M) * D.invT64 - c0;
   auto visit = [&](float z) {
-    const float bf = fmaf(z, hk.kz, hk.k0);
-    if (!(bf < static_cast<float>(kHB))) return;  // beyond 50 nats below A0, -inf, NaN
-    int b;
-    if (bf >= 0.0f) {
-      b = static_cast<int>(bf);
-      if (SPARSE && b > b_hi) return;  // below the window: estimated from the histogram
-    } else {
-      b = -1;  // the list above the bins
-    }
+    const float x = fmaf(z, hk.kz4, hk.k04);
+    if (!(x < static_cast<float>(kHB) * kOffQ)) return;  // beyond 50 nats below A0, -inf, NaN
     const double u = fma(static_cast<double>(z), D.invT64, nMTc);
     double e;
-    if (b >= 0) {
+    int b;
+    if (x >= 0.0f) {
+      b = static_cast<int>(static_cast<uint32_t>(x) >> kOffBits);
+      if (SPARSE && b > b_hi) return;  // below the window: estimated from the histogram
       const double r = fma(static_cast<double>(b), invK, u);
       const float rf = static_cast<float>(r);
       const float cf = fmaf(rf, fmaf(rf, 1.0f / 120.0f, 1.0f / 24.0f), 1.0f / 6.0f);
@@ -632,6 +627,7 @@ __device__ bool exact_cut(const void* row, int32_t V, int64_t h, int64_t nvec, c
       q = fma(q, r, 1.0);
       e = sh.u.wtab[b] * q;
     } else {
+      b = -1;  // the list above the bins
       e = exp_tang(fmax(u + c0, -700.0), tab);
     }
     if (!SPARSE) sT += e;
@@ -741,7 +737,7 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   // one while |k0| < 2^18 (kz and k0 carry a relative error below 2.4e-7,
   // and a binned logit has |z kz| < |k0| + kHB): every binned logit then
   // lies within 0.012 nats of its bin centre, where the exact pass's
-  // degree-5 polynomial is accurate to 3e-15. Rows with larger |A0| / T
+  // degree-5 polynomial is accurate to 3e-14. Rows with larger |A0| / T
   // (beyond about 4,800) take the three-pass method.
   if (!(fabsf(hk.k0) < 0x1p18f)) return false;
 
@@ -769,8 +765,9 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   auto bin_mass = [&](int b, double w) -> double {
     const uint64_t word = sh.u.hs.bins[b];
     const double cnt = static_cast<double>(static_cast<uint32_t>(word >> kCountShift));
+    // a position p stands for the offset (p + 1/2) / kOffQ - 1/2 from the centre
     const double dsum =
-        (static_cast<double>(word & ((uint64_t{1} << kCountShift) - 1)) - cnt * (0.5 * kOffQ)) * (1.0 / kOffQ);
+        (static_cast<double>(word & ((uint64_t{1} << kCountShift) - 1)) - cnt * (0.5 * kOffQ - 0.5)) * (1.0 / kOffQ);
     return fma(-dsum, hb, cnt) * w;
   };
   double sa = 0.0;
@@ -847,8 +844,8 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   // most half a bin (0.0092 nats) plus the float32 rounding of bf (see
   // above): the degree-5 Taylor polynomial 1 + r + r^2 / 2 + r^3 c(r), c(r)
   // = 1/6 + r/24 + r^2/120 taken in float32 (its rounding, below 1.5e-8,
-  // moves the polynomial by less than |r|^3 1.5e-8 < 3e-14). The list
-  // takes the table-driven exp.
+  // moves the polynomial by less than |r|^3 1.5e-8 < 3e-14; the remainder
+  // r^6 / 720 is below 4.2e-15). The list takes the table-driven exp.
   const double lead0 = (static_cast<double>(A0) - static_cast<double>(D.M)) * D.invT64 + kHAbove;
   const double c0 = lead0 - 0.5 * invK;  // centre of bin b: c0 - b * invK
   {
@@ -861,7 +858,7 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
 
   // Sparse pass when few lanes have three buckets reaching the window: a
   // bucket can reach it only if its maximum does (bf falls with z).
-  auto reaches = [&](float x) { return fmaf(x, hk.kz, hk.k0) < static_cast<float>(W.b_hi + 1); };
+  auto reaches = [&](float x) { return fmaf(x, hk.kz4, hk.k04) < static_cast<float>(W.b_hi + 1) * kOffQ; };
   const bool full = reaches(tk.b3);
   const int64_t s1 = (tk.b1v >= 0 && reaches(tk.b1)) ? tk.b1v : -1;
   const int64_t s2 = (tk.b2v >= 0 && reaches(tk.b2)) ? tk.b2v : -1;
@@ -960,7 +957,7 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
     for (int k = 0; k < VEC; ++k) pm = fmaxf(pm, z[k]);
   }
   pm = wave_max(pm);
-  for (int b = threadIdx.x; b < kHB + kWave; b += kTpBlock) sh.u.hs.bins[b] = 0;
+  for (int b = threadIdx.x; b < kHB; b += kTpBlock) sh.u.hs.bins[b] = 0;
   if (threadIdx.x < 64) sh.exptab[threadIdx.x] = exp2(static_cast<double>(threadIdx.x) * (1.0 / 64.0));
   if (threadIdx.x == 0) sh.n_above = 0;
   if (threadIdx.x % kWave == 0) sh.red_f[threadIdx.x / kWave] = pm;
@@ -983,9 +980,10 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
   hk.bins = sh.u.hs.bins;
   hk.above = sh.above;
   hk.n_above = &sh.n_above;
-  hk.discard = kHB + static_cast<int32_t>(threadIdx.x % kWave);
   hk.kz = anchored ? -invT * kHK : 0.0f;
   hk.k0 = anchored ? fmaf(A0, invT * kHK, kHAbove * kHK) : INFINITY;  // unanchored: nothing binned
+  hk.kz4 = hk.kz * kOffQ;
+  hk.k04 = hk.k0 * kOffQ;
 
   // 1. stats pass, building the histogram (S and E of the merged state are
   // only formed for a row without a nucleus)
