@@ -530,7 +530,7 @@ __device__ __forceinline__ uint32_t row_flags(const RowArgs& a, int64_t r, const
 // nucleus, the distribution features are those of the renormalised nucleus.
 // Fills the confidence tuple A = (logprob, maxprob, -entropy, margin) and
 // returns the row's flags.
-__device__ uint32_t finalize_row(const RowArgs& a, int64_t r, const Partial& p, const RowCtx& cx, uint32_t fix,
+__device__ __forceinline__ uint32_t finalize_row(const RowArgs& a, int64_t r, const Partial& p, const RowCtx& cx, uint32_t fix,
                                  float* conf, const Nucleus* nuc = nullptr) {
   const float T = cx.T;
   uint32_t flags = row_flags(a, r, p, T);

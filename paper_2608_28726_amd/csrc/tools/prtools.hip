@@ -1,7 +1,8 @@
 // Workload tools for tests and benchmarks, built as libprtools.so: the seeded
-// logit-row generator and a read-only HBM bandwidth probe. Neither is part of
-// the verifier's interface (include/prouter.h) and neither computes anything
-// the verifier computes.
+// logit-row generator, a read-only HBM bandwidth probe and an exhaustive
+// accuracy check of the hardware exp2. None is part of the verifier's
+// interface (include/prouter.h) and none computes anything the verifier
+// computes.
 //
 // The generator is the device twin of the numpy generator in
 // paper_2608_28726_amd/workloads.py: both take the same integer and float32
@@ -138,6 +139,42 @@ __global__ void __launch_bounds__(256) read_probe_kernel(const vec4u* __restrict
   if (acc == 0x9E3779B9u) sink[gid] = acc;
 }
 
+// Largest relative error of the hardware base-2 exponential (v_exp_f32) over
+// every float x in [lo, hi], against the float64 exp2: the bound the top-p
+// kernel's float32 pass certifies its masses with. out[0] receives the bits
+// of the largest error (a non-negative double), out[1] the bits of an input
+// at which it occurs. Each thread walks a strided share of the 2^32 bit
+// patterns; one atomic per wave.
+__global__ void __launch_bounds__(256) exp2_error_kernel(float lo, float hi, unsigned long long* out) {
+  const uint64_t n = uint64_t{1} << 32;
+  const uint64_t step = static_cast<uint64_t>(gridDim.x) * blockDim.x;
+  unsigned long long worst = 0, wx = 0;
+  for (uint64_t i = static_cast<uint64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += step) {
+    const uint32_t b = static_cast<uint32_t>(i);
+    const float x = __uint_as_float(b);
+    if (!(x >= lo && x <= hi)) continue;
+    const double r = exp2(static_cast<double>(x));
+    const double e = fabs(static_cast<double>(__builtin_amdgcn_exp2f(x)) - r) / r;
+    const unsigned long long eb = static_cast<unsigned long long>(__double_as_longlong(e));
+    if (eb > worst) {
+      worst = eb;
+      wx = b;
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) {  // wave maximum (non-negative doubles order as integers)
+    const unsigned long long o = __shfl_xor(worst, off);
+    const unsigned long long ox = __shfl_xor(wx, off);
+    if (o > worst) {
+      worst = o;
+      wx = ox;
+    }
+  }
+  if (threadIdx.x % 64 == 0) {
+    const unsigned long long old = atomicMax(&out[0], worst);
+    if (worst > old) atomicExch(&out[1], wx);
+  }
+}
+
 }  // namespace
 
 extern "C" {
@@ -189,6 +226,15 @@ int prt_read_probe(const void* buf, int64_t nbytes, uint32_t* sink, int32_t bloc
     hipLaunchKernelGGL(read_probe_kernel<16>, grid, dim3(256), 0, st, p, nbytes / 16, sink);
   else
     return 1;
+  return hipGetLastError() == hipSuccess ? 0 : 3;
+}
+
+// Runs the exp2 accuracy check above over [lo, hi] (finite, lo <= hi). out is
+// a device array of two zeroed 64-bit words. Returns 0, 1 (bad argument) or
+// 3 (launch failure).
+int prt_exp2_max_rel_err(float lo, float hi, unsigned long long* out, void* stream) {
+  if (!out || !(lo <= hi) || !(lo > -INFINITY) || !(hi < INFINITY)) return 1;
+  hipLaunchKernelGGL(exp2_error_kernel, dim3(4096), dim3(256), 0, static_cast<hipStream_t>(stream), lo, hi, out);
   return hipGetLastError() == hipSuccess ? 0 : 3;
 }
 

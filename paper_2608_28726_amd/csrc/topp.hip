@@ -61,6 +61,16 @@ constexpr double kWinMargin = 5e-4;  // relative margin of the window around P *
 constexpr int kOffBits = 12;         // fixed-point bits of a logit's position inside its bin
 constexpr float kOffQ = 4096.0f;     // 2^kOffBits
 constexpr int kCountShift = 40;      // a histogram word: count << kCountShift | offset sum
+constexpr double kLog2eD = 1.4426950408889634;  // log2(e)
+constexpr double kLn2D = 0.6931471805599453;    // ln(2)
+#ifndef PR_APPROX_LDX
+#define PR_APPROX_LDX 4  // loads per lane in flight in the float32 pass
+#endif
+// Relative error bound of the hardware exp2 (v_exp_f32) for arguments in
+// [-100, 1]; its largest error over every float there is 8.49e-8 (a GPU test
+// re-checks the whole range).
+constexpr double kExp2RelErr = 1.0e-7;
+constexpr double kTSlack = 0.05;  // the float32 pass's frame: see approx_cut
 
 struct TpShared {
   union {
@@ -97,12 +107,12 @@ struct TpShared {
 };
 
 // Calls fn(z) for every logit of the row (order irrelevant), with the
-// double-buffered loop of the scan (lanes past the end see -inf, which every
-// fn ignores).
-template <typename Tin, typename Fn>
+// double-buffered loop of the scan, LDX vector loads per lane in flight
+// (lanes past the end see -inf, which every fn ignores).
+template <typename Tin, int LDX = 2, typename Fn>
 __device__ __forceinline__ void for_each_logit(const void* row, int32_t V, int64_t h, int64_t nvec, Fn fn) {
   constexpr int VEC = Elem<Tin>::kVec;
-  constexpr int LDX = 2, UX = 1;
+  constexpr int UX = 1;
   const int t = threadIdx.x;
   if (t < h) fn(Elem<Tin>::load1(row, t));
   const vec4u* vp = reinterpret_cast<const vec4u*>(static_cast<const Tin*>(row) + h);
@@ -121,7 +131,7 @@ __device__ __forceinline__ void for_each_logit(const void* row, int32_t V, int64
 }
 
 // Block-wide sums of (x, y) in a fixed order; every thread gets the result.
-__device__ void block_sum2(double& x, double& y, TpShared& sh) {
+__device__ __forceinline__ void block_sum2(double& x, double& y, TpShared& sh) {
   x = wave_sum_d(x);
   y = wave_sum_d(y);
   const int w = threadIdx.x / kWave;
@@ -140,7 +150,7 @@ __device__ void block_sum2(double& x, double& y, TpShared& sh) {
   __syncthreads();
 }
 
-__device__ uint32_t block_sum_u(uint32_t v, TpShared& sh) {
+__device__ __forceinline__ uint32_t block_sum_u(uint32_t v, TpShared& sh) {
   v = wave_sum_u(v);
   __syncthreads();
   if (threadIdx.x % kWave == 0) sh.red_u[threadIdx.x / kWave] = v;
@@ -152,7 +162,7 @@ __device__ uint32_t block_sum_u(uint32_t v, TpShared& sh) {
 }
 
 // Exclusive block scan of one double per thread (thread order).
-__device__ double block_exclusive_scan(double v, TpShared& sh) {
+__device__ __forceinline__ double block_exclusive_scan(double v, TpShared& sh) {
   const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
   double incl = v;
 #pragma unroll
@@ -253,7 +263,7 @@ struct HistHook {
 };
 
 // Bitonic sort of sh.win[0..n2) into descending order (n2 a power of two).
-__device__ void bitonic_desc(float* a, int n2) {
+__device__ __forceinline__ void bitonic_desc(float* a, int n2) {
   for (int size = 2; size <= n2; size <<= 1) {
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
       for (int i = threadIdx.x; i < (n2 >> 1); i += kTpBlock) {
@@ -583,6 +593,82 @@ __device__ __forceinline__ void for_each_listed_logit(const void* row, int32_t V
     if (ok[u]) body(x[u]);
 }
 
+// Step 3 of the histogram method: the window's nw_all logits (in sh.win)
+// sorted into descending order and scanned. A logit's mass is exp(dd(z)) in
+// the caller's frame; mA and eA are the mass and the entropy sum (nats of
+// that frame) above the window, cA the number of logits there. The cutoff
+// is the first index j at which the running mass mA + C_j reaches the
+// target; thr(wm, t_lo, t_hi) gives the interval [t_lo, t_hi] the target
+// may lie in (wm: the window's total mass), and j is taken only where both
+// ends give the same index. Returns false when they do not, or when the
+// crossing lies outside the window; else the nucleus size and its mass and
+// entropy sums in the caller's frame.
+template <typename DD, typename Thr>
+__device__ bool cut_window(TpShared& sh, uint32_t nw_all, uint32_t cA, double mA, double eA, DD dd_of, Thr thr,
+                           Nucleus& nuc) {
+  const double* tab = sh.exptab;
+  const int nw = static_cast<int>(nw_all);
+  int n2 = 2;
+  while (n2 < nw) n2 <<= 1;
+  for (int i = nw + threadIdx.x; i < n2; i += kTpBlock) sh.win[i] = -INFINITY;
+  __syncthreads();
+  bitonic_desc(sh.win, n2);
+  const int per = (n2 + kTpBlock - 1) / kTpBlock;
+  const int i0 = threadIdx.x * per;
+  const int i1 = i0 + per < nw ? i0 + per : nw;
+  double sm = 0.0, se = 0.0;
+  for (int i = i0; i < i1; ++i) {
+    const double dd = dd_of(sh.win[i]);
+    const double e = exp_tang(dd, tab);
+    sm += e;
+    se += e * dd;
+  }
+  const double cm = block_exclusive_scan(sm, sh);
+  const double ce = block_exclusive_scan(se, sh);
+  double wm = sm, we = se;
+  block_sum2(wm, we, sh);
+  double t_lo, t_hi;
+  thr(wm, t_lo, t_hi);
+  if (!(mA < t_lo) || mA + wm < t_hi) return false;  // crossing outside the window
+  if (threadIdx.x == 0) {
+    sh.jfirst = 0xffffffffu;
+    sh.rdigit = 0xffffffffu;  // the first index reaching t_hi
+  }
+  __syncthreads();
+  double run_m = mA + cm;
+  bool lo_found = false;
+  for (int i = i0; i < i1; ++i) {
+    run_m += exp_tang(dd_of(sh.win[i]), tab);
+    if (!lo_found && run_m >= t_lo) {
+      atomicMin(&sh.jfirst, static_cast<uint32_t>(i));
+      lo_found = true;
+    }
+    if (run_m >= t_hi) {
+      atomicMin(&sh.rdigit, static_cast<uint32_t>(i));
+      break;
+    }
+  }
+  __syncthreads();
+  const uint32_t jf = sh.jfirst;
+  if (jf == 0xffffffffu || jf != sh.rdigit) return false;  // not decided within the bound
+  if (static_cast<int>(jf) >= i0 && static_cast<int>(jf) < i1) {
+    double m2 = mA + cm, e2 = eA + ce;
+    for (int i = i0; i <= static_cast<int>(jf); ++i) {
+      const double dd = dd_of(sh.win[i]);
+      const double e = exp_tang(dd, tab);
+      m2 += e;
+      e2 += e * dd;
+    }
+    sh.SN = m2;
+    sh.EN = e2;
+  }
+  __syncthreads();
+  nuc.k = static_cast<int32_t>(cA + jf + 1);
+  nuc.S = sh.SN;
+  nuc.E = sh.EN;
+  return true;
+}
+
 // Steps 2 and 3 of the histogram method: the exact pass over the row (dense)
 // or over the buckets that can reach the window (sparse), the window sorted
 // and scanned. Dense: S is the float64 total over every binned logit.
@@ -593,7 +679,7 @@ __device__ __forceinline__ void for_each_listed_logit(const void* row, int32_t V
 // window. Returns false when the method cannot decide (the caller then tries
 // the dense pass, then the three-pass method).
 template <typename Tin, bool SPARSE>
-__device__ bool exact_cut(const void* row, int32_t V, int64_t h, int64_t nvec, const Dist& D, float P,
+__device__ __forceinline__ bool exact_cut(const void* row, int32_t V, int64_t h, int64_t nvec, const Dist& D, float P,
                           const HistHook& hk, TpShared& sh, const Window& W, double c0, double invK, bool full,
                           int64_t s1, int64_t s2, Nucleus& nuc) {
   const double* tab = sh.exptab;
@@ -656,70 +742,106 @@ __device__ bool exact_cut(const void* row, int32_t V, int64_t h, int64_t nvec, c
     if (nA_all != cA || nw_all != W.inwin) return false;
   }
 
-  // 3. sort the window (descending), scan its masses, verify the crossing
-  const int nw = static_cast<int>(nw_all);
-  int n2 = 2;
-  while (n2 < nw) n2 <<= 1;
-  for (int i = nw + threadIdx.x; i < n2; i += kTpBlock) sh.win[i] = -INFINITY;
+  return cut_window(
+      sh, nw_all, cA, mA, eA, [&](float z) { return D.d64(z); },
+      [&](double wm, double& t_lo, double& t_hi) {
+        // The total and the range the target P * S may lie in: exact (to
+        // float64 rounding) in the dense pass, the histogram estimate's bound
+        // in the sparse one.
+        const double S = SPARSE ? mA + wm + W.s_below : sT2;
+        const double err = SPARSE ? W.s_below_err + 1e-13 * S : 0.0;
+        t_lo = static_cast<double>(P) * (S - err);
+        t_hi = static_cast<double>(P) * (S + err);
+      },
+      nuc);
+}
+
+// Step 2 in float32, for rows whose window many buckets reach (the flat
+// ones). One pass forms every binned logit's mass as 2^t, t = z c + nMc with
+// c = log2(e) / T held as a float pair (two fmas) and nMc = -M c + shift
+// rounded to float (the frame: every mass carries the common factor 2^tau,
+// tau = nMc + M c; the shift puts t = 0 at the window), by the hardware
+// exp2; float64 sums of the masses and of m t over every binned logit and
+// over those above the window; the window gathered. The window's masses are then taken exactly (float64) in
+// the same frame, and the cutoff only where the certified error of the
+// float32 masses leaves one index. The bound: a logit's t errs by at most
+// 2^-23 |t| + 2^-47 max|z| c (two roundings of |t| and the float pair's
+// remainder), so its mass by ln2 (2^-23 |t| + 2^-47 max|z| c) + kExp2RelErr
+// relative (for t >= -100; below, at most 2^-100 absolute). With mass
+// errors d_A above the window and d_R in the rest (window included, since
+// the total is the float32 sum), the test quantity mA + C_j - P S errs by at
+// most (1 - P) d_A + P d_R. Returns false when that does not decide (the
+// caller then takes the float64 pass); else the nucleus relative to M.
+template <typename Tin>
+__device__ __forceinline__ bool approx_cut(const void* row, int32_t V, int64_t h, int64_t nvec, const Dist& D, float P, float A0,
+                           const HistHook& hk, TpShared& sh, const Window& W, Nucleus& nuc) {
+  if (threadIdx.x == 0) sh.wcount = 0;
   __syncthreads();
-  bitonic_desc(sh.win, n2);
-  const int per = (n2 + kTpBlock - 1) / kTpBlock;
-  const int i0 = threadIdx.x * per;
-  const int i1 = i0 + per < nw ? i0 + per : nw;
-  double sm = 0.0, se = 0.0;
-  for (int i = i0; i < i1; ++i) {
-    const double dd = D.d64(sh.win[i]);
-    const double e = exp_tang(dd, tab);
-    sm += e;
-    se += e * dd;
-  }
-  const double cm = block_exclusive_scan(sm, sh);
-  const double ce = block_exclusive_scan(se, sh);
-  double wm = sm, we = se;
-  block_sum2(wm, we, sh);
-  // The total and the range the target P * S may lie in: exact (to float64
-  // rounding) in the dense pass, the histogram estimate's bound in the sparse one.
-  const double S = SPARSE ? mA + wm + W.s_below : sT2;
-  const double err = SPARSE ? W.s_below_err + 1e-13 * S : 0.0;
-  const double t_lo = static_cast<double>(P) * (S - err);
-  const double t_hi = static_cast<double>(P) * (S + err);
-  if (!(mA < t_lo) || mA + wm < t_hi) return false;  // crossing outside the window
-  if (threadIdx.x == 0) {
-    sh.jfirst = 0xffffffffu;
-    sh.rdigit = 0xffffffffu;  // the first index reaching t_hi
-  }
-  __syncthreads();
-  double run_m = mA + cm;
-  bool lo_found = false;
-  for (int i = i0; i < i1; ++i) {
-    run_m += exp_tang(D.d64(sh.win[i]), tab);
-    if (!lo_found && run_m >= t_lo) {
-      atomicMin(&sh.jfirst, static_cast<uint32_t>(i));
-      lo_found = true;
+  const double c64 = kLog2eD * D.invT64;
+  const float c_hi = static_cast<float>(c64);
+  const float c_lo = static_cast<float>(c64 - static_cast<double>(c_hi));
+  // The frame puts t = 0 near the window (bin b_lo's centre, at most 100
+  // above M's t): the rounding error of t grows with |t|, and the logits
+  // that decide the cutoff are the massive ones and those near the window.
+  const double zw = W.b_lo >= 0 ? (static_cast<double>(W.b_lo) + 0.5 - static_cast<double>(hk.k0)) /
+                                      static_cast<double>(hk.kz)
+                                : static_cast<double>(D.M);
+  const double shift = fmin((static_cast<double>(D.M) - zw) * c64, 100.0);
+  const float nMc = static_cast<float>(-static_cast<double>(D.M) * c64 + fmax(shift, 0.0));
+  const double nMc64 = static_cast<double>(nMc);
+  const float xa = W.b_lo >= 0 ? static_cast<float>(W.b_lo) * kOffQ : -INFINITY;  // above the window: x < xa
+  const float xb = static_cast<float>(W.b_hi + 1) * kOffQ;                       // in it: xa <= x < xb
+  double sT = 0.0, tT = 0.0, mA = 0.0, tA = 0.0;
+  auto visit = [&](float z) {
+    const float x = fmaf(z, hk.kz4, hk.k04);
+    if (!(x < static_cast<float>(kHB) * kOffQ)) return;  // the binned logits, as in the exact pass
+    const float t = fmaf(z, c_lo, fmaf(z, c_hi, nMc));
+    const float e = __builtin_amdgcn_exp2f(t);
+    const double e64 = static_cast<double>(e);
+    const double et = e64 * static_cast<double>(t);  // exact
+    sT += e64;
+    tT += et;
+    if (x < xa) {
+      mA += e64;
+      tA += et;
+    } else if (x < xb) {
+      const uint32_t slot = atomicAdd(&sh.wcount, 1u);
+      if (slot < static_cast<uint32_t>(kCap)) sh.win[slot] = z;
     }
-    if (run_m >= t_hi) {
-      atomicMin(&sh.rdigit, static_cast<uint32_t>(i));
-      break;
-    }
-  }
-  __syncthreads();
-  const uint32_t jf = sh.jfirst;
-  if (jf == 0xffffffffu || jf != sh.rdigit) return false;  // not decided within the bound
-  if (static_cast<int>(jf) >= i0 && static_cast<int>(jf) < i1) {
-    double m2 = mA + cm, e2 = eA + ce;
-    for (int i = i0; i <= static_cast<int>(jf); ++i) {
-      const double dd = D.d64(sh.win[i]);
-      const double e = exp_tang(dd, tab);
-      m2 += e;
-      e2 += e * dd;
-    }
-    sh.SN = m2;
-    sh.EN = e2;
-  }
-  __syncthreads();
-  nuc.k = static_cast<int32_t>(cA + jf + 1);
-  nuc.S = sh.SN;
-  nuc.E = sh.EN;
+  };
+  for_each_logit<Tin, PR_APPROX_LDX>(row, V, h, nvec, visit);
+  block_sum2(sT, tT, sh);
+  block_sum2(mA, tA, sh);
+  const uint32_t nw_all = sh.wcount;
+  if (nw_all > static_cast<uint32_t>(kCap) || nw_all != W.inwin) return false;
+  // the bound (sums of the float32 masses, inflated for their own error)
+  const double T = 1.0 / D.invT64;
+  const double zc = fmax(fabs(static_cast<double>(D.M)), fabs(static_cast<double>(A0)) + 50.0 * T) * c64;
+  const double g1 = kLn2D * 0x1p-23 * 1.0001;                           // per unit of m |t|
+  const double g0 = (kLn2D * 0x1p-47 * zc + kExp2RelErr) * 1.0001;     // per unit of m
+  // sums of m |t|: in this frame a logit above the window has t > -kTSlack
+  // and any other one t < kTSlack (half a bin is 0.0132 in t, plus the
+  // roundings of the bin coordinate and of nMc)
+  const double aA = tA + 2.0 * kTSlack * mA;                     // above the window
+  const double aR = (tA - tT) + 2.0 * kTSlack * (sT - mA);       // the rest
+  const double d_above = (g1 * aA + g0 * mA) * (1.0 + 1e-6);
+  const double d_rest = (g1 * aR + g0 * (sT - mA)) * (1.0 + 1e-6);
+  const double Pd = static_cast<double>(P);
+  const double dF = (1.0 - Pd) * d_above + Pd * fmax(d_rest, 0.0) + static_cast<double>(V) * (0x1p-99 + 2e-22) +
+                    1e-12 * sT;
+  const double tau_n = kLn2D * (nMc64 + static_cast<double>(D.M) * c64);  // the frame's offset, in nats
+  const bool ok = cut_window(
+      sh, nw_all, W.above, mA, kLn2D * tA, [&](float z) { return kLn2D * fma(static_cast<double>(z), c64, nMc64); },
+      [&](double, double& t_lo, double& t_hi) {
+        t_lo = Pd * sT - dF;
+        t_hi = Pd * sT + dF;
+      },
+      nuc);
+  if (!ok) return false;
+  // from the frame to masses relative to M: m_M = m / e^tau_n, d_M = d - tau_n
+  const double inv_kappa = exp(-tau_n);
+  nuc.E = (nuc.E - tau_n * nuc.S) * inv_kappa;
+  nuc.S *= inv_kappa;
   return true;
 }
 
@@ -866,6 +988,7 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   if (n_full <= kSparseFullLanes &&
       exact_cut<Tin, true>(row, V, h, nvec, D, P, hk, sh, W, c0, invK, full, s1, s2, nuc))
     return true;
+  if (approx_cut<Tin>(row, V, h, nvec, D, P, A0, hk, sh, W, nuc)) return true;
   return exact_cut<Tin, false>(row, V, h, nvec, D, P, hk, sh, W, c0, invK, true, -1, -1, nuc);
 }
 

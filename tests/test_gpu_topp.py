@@ -166,3 +166,46 @@ def test_topp_bf16_large_vocabulary():
     assert logits.dtype == torch.bfloat16
     print(f"case topp bf16 V=151936 rows={b.n_rows}", flush=True)
     compare_features(gpu_features(logits, ids, T, P), oracle_features(logits, ids, T, P))
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_topp_flat_rows(dtype):
+    """Flat and near-flat rows (sigma / T from 0.02 to 2, P from 0.5 to 0.99):
+    the rows whose window many buckets reach, which take the float32 pass
+    with its certified bound (and the float64 pass where the bound does not
+    decide), against the oracle's exact cutoff."""
+    V = 131072
+    rng = np.random.default_rng(2024)
+    n = 32
+    sig = np.geomspace(0.02, 2.0, n)
+    T = rng.uniform(0.5, 1.5, n)
+    z = rng.normal(0, 1, (n, V)) * (sig * T)[:, None] + rng.uniform(-5, 5, (n, 1))
+    P = rng.uniform(0.5, 0.99, n)
+    ids = rng.integers(0, V, n)
+    logits, ids, T, P = _run(z, ids, T, P, dtype)
+    print(f"case topp flat rows V={V} {dtype}", flush=True)
+    compare_features(gpu_features(logits, ids, T, P), oracle_features(logits, ids, T, P))
+
+
+def test_hardware_exp2_bound():
+    """The float32 pass of the top-p kernel certifies its masses with a bound
+    of 1e-7 on the relative error of the hardware exp2 (the constant
+    kExp2RelErr) for arguments in [-100, 100] (its frame keeps t there):
+    checked here over every float in [-126, 127]."""
+    out = torch.zeros(2, dtype=torch.int64, device="cuda")
+    st = wl.tools().prt_exp2_max_rel_err(-126.0, 127.0, out.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    assert st == 0
+    torch.cuda.synchronize()
+    w = out.cpu().numpy()
+    err = float(w[:1].view(np.float64)[0])
+    x = float(np.array([w[1]], dtype=np.int64).astype(np.uint32).view(np.float32)[0])
+    print(f"case exp2 bound: largest relative error {err:.4e} (at x = {x:.9g})", flush=True)
+    assert 0.0 < err <= 1.0e-7
+    # a sub-range reports a largest error inside it, no larger than the whole range's
+    out.zero_()
+    assert wl.tools().prt_exp2_max_rel_err(-1.0, 1.0, out.data_ptr(), torch.cuda.current_stream().cuda_stream) == 0
+    torch.cuda.synchronize()
+    w = out.cpu().numpy()
+    e1 = float(w[:1].view(np.float64)[0])
+    x1 = float(np.array([w[1]], dtype=np.int64).astype(np.uint32).view(np.float32)[0])
+    assert -1.0 <= x1 <= 1.0 and 0.0 < e1 <= err
