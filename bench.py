@@ -657,8 +657,8 @@ KERNEL_SOURCES = {
                             "paper_2608_28726_amd/csrc/sample.h", "paper_2608_28726_amd/csrc/row_features.hip"),
     "topp_kernel": ("include/prouter.h", "paper_2608_28726_amd/csrc/device_util.h",
                     "paper_2608_28726_amd/csrc/row_features.h", "paper_2608_28726_amd/csrc/row_scan.h",
-                    "paper_2608_28726_amd/csrc/topk.h", "paper_2608_28726_amd/csrc/topp.h",
-                    "paper_2608_28726_amd/csrc/topp.hip"),
+                    "paper_2608_28726_amd/csrc/topk.h", "paper_2608_28726_amd/csrc/p2.h",
+                    "paper_2608_28726_amd/csrc/topp.h", "paper_2608_28726_amd/csrc/topp.hip"),
 }
 
 
