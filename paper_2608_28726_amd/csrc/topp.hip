@@ -593,6 +593,126 @@ __device__ __forceinline__ void for_each_listed_logit(const void* row, int32_t V
     if (ok[u]) body(x[u]);
 }
 
+// Inclusive prefix sum over the lanes of a wave, in a fixed order.
+__device__ __forceinline__ double wave_incl_scan_d(double x) {
+  const int lane = static_cast<int>(threadIdx.x % kWave);
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const double t = __shfl_up(x, d);
+    if (lane >= d) x += t;
+  }
+  return x;
+}
+
+// Sorts the 512 floats a wave holds, 8 per lane (element 8 lane + k), into
+// descending order with the same bitonic network as bitonic_desc: strides
+// below 8 compare registers of one lane, longer ones the same register of
+// lane ^ (stride / 8).
+__device__ __forceinline__ void wave_bitonic_desc512(float (&v)[8]) {
+  const int lane = static_cast<int>(threadIdx.x % kWave);
+#pragma unroll
+  for (int size = 2; size <= 512; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      if (stride >= 8) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int i = 8 * lane + k;
+          const float p = __shfl_xor(v[k], stride >> 3);
+          const bool keep_max = ((i & size) == 0) == ((i & stride) == 0);
+          v[k] = keep_max ? fmaxf(v[k], p) : fminf(v[k], p);
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          if (k & stride) continue;
+          const bool desc = ((8 * lane + k) & size) == 0;
+          const float a = v[k], b = v[k | stride];
+          v[k] = desc ? fmaxf(a, b) : fminf(a, b);
+          v[k | stride] = desc ? fminf(a, b) : fmaxf(a, b);
+        }
+      }
+    }
+  }
+}
+
+// cut_window for a window of at most 512 logits: wave 0 holds it in
+// registers, sorts it, forms each mass once and scans with wave prefix sums
+// (no workgroup barrier until the result is published). Same result as the
+// workgroup-wide version up to the order of float64 additions.
+template <typename DD, typename Thr>
+__device__ __forceinline__ bool cut_window_wave(TpShared& sh, int nw, uint32_t cA, double mA, double eA, DD dd_of,
+                                                Thr thr, Nucleus& nuc) {
+  const double* tab = sh.exptab;
+  if (threadIdx.x < kWave) {
+    const int lane = static_cast<int>(threadIdx.x);
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = 8 * lane + k < nw ? sh.win[8 * lane + k] : -INFINITY;
+    wave_bitonic_desc512(v);
+    double e[8], ed[8];
+    double ls = 0.0, le = 0.0;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      e[k] = 0.0;
+      ed[k] = 0.0;
+      if (8 * lane + k < nw) {  // the window's logits lead the sorted order (the padding is -inf)
+        const double dd = dd_of(v[k]);
+        e[k] = exp_tang(dd, tab);
+        ed[k] = e[k] * dd;
+      }
+      ls += e[k];
+      le += ed[k];
+    }
+    const double is = wave_incl_scan_d(ls), ie = wave_incl_scan_d(le);
+    // sums over the lanes before this one (the shuffles run in every lane: a
+    // shuffle must not read a lane that is not executing it)
+    const double pis = __shfl_up(is, 1), pie = __shfl_up(ie, 1);
+    const double cm = lane > 0 ? pis : 0.0;
+    const double ce = lane > 0 ? pie : 0.0;
+    const double wm = __shfl(is, kWave - 1);
+    double t_lo, t_hi;
+    thr(wm, t_lo, t_hi);
+    constexpr int kNone = 1 << 30;
+    int jlo = kNone, jhi = kNone;
+    const bool inside = mA < t_lo && !(mA + wm < t_hi);  // else the crossing lies outside the window
+    if (inside) {
+      double run = mA + cm;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        run += e[k];
+        if (jlo == kNone && run >= t_lo) jlo = 8 * lane + k;
+        if (jhi == kNone && run >= t_hi) jhi = 8 * lane + k;
+      }
+    }
+    // indices grow with the lane: the first lane that has one holds the smallest
+    const uint64_t mlo = __ballot(jlo != kNone), mhi = __ballot(jhi != kNone);
+    const int jf = mlo ? __shfl(jlo, static_cast<int>(__builtin_ctzll(mlo))) : kNone;
+    const int jr = mhi ? __shfl(jhi, static_cast<int>(__builtin_ctzll(mhi))) : kNone;
+    const bool decided = inside && jf != kNone && jf == jr;
+    if (decided && jf / 8 == lane) {
+      double m2 = mA + cm, e2 = eA + ce;
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        if (k <= jf % 8) {
+          m2 += e[k];
+          e2 += ed[k];
+        }
+      }
+      sh.SN = m2;
+      sh.EN = e2;
+    }
+    if (lane == 0) sh.jfirst = decided ? static_cast<uint32_t>(jf) : 0xffffffffu;
+  }
+  __syncthreads();
+  const uint32_t jf = sh.jfirst;
+  if (jf == 0xffffffffu) return false;
+  nuc.k = static_cast<int32_t>(cA + jf + 1);
+  nuc.S = sh.SN;
+  nuc.E = sh.EN;
+  return true;
+}
+
 // Step 3 of the histogram method: the window's nw_all logits (in sh.win)
 // sorted into descending order and scanned. A logit's mass is exp(dd(z)) in
 // the caller's frame; mA and eA are the mass and the entropy sum (nats of
@@ -608,6 +728,7 @@ __device__ bool cut_window(TpShared& sh, uint32_t nw_all, uint32_t cA, double mA
                            Nucleus& nuc) {
   const double* tab = sh.exptab;
   const int nw = static_cast<int>(nw_all);
+  if (nw <= 512) return cut_window_wave(sh, nw, cA, mA, eA, dd_of, thr, nuc);
   int n2 = 2;
   while (n2 < nw) n2 <<= 1;
   for (int i = nw + threadIdx.x; i < n2; i += kTpBlock) sh.win[i] = -INFINITY;
