@@ -268,8 +268,8 @@ size_t pr_verifier_head_workspace(int64_t n_rows);
  *   offsets    int32 [n_req + 1], device; precondition as for
  *              pr_request_aggregate.
  *   max_len    at least the number of tokens of the longest request; a
- *              longer request scores NaN (the attention grid is sized by it).
- *              1 .. 2^20 (PR_ERR_UNSUPPORTED above).
+ *              longer request scores NaN. 1 .. 2^20 (PR_ERR_UNSUPPORTED
+ *              above).
  *   weights    float [PR_HEAD_WEIGHTS], device, 16-byte aligned, in this order (matrices
  *              row-major [out][in]): W_in [64][4], b_in [64]; per layer:
  *              W_qkv [192][64] (query rows, then key rows, then value rows;

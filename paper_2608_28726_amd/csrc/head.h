@@ -19,9 +19,12 @@ struct HeadArgs {
   int32_t max_len;         // longest request the attention grid covers
   const float* weights;    // [kHeadWeights]
   float* scores;           // [n_req]
-  float* ws;               // workspace: H0, H1 [n_rows][64], qkv [n_rows][192], att [n_rows][64]
+  float* ws;               // workspace: H0, H1 [n_rows][64], qkv [n_rows][192], att [n_rows][64],
+                           // then the attention work list and its counters
   float* qkv;              // set by launch_head
   float* att;              // set by launch_head
+  int32_t* items;          // set by launch_head: [2][n_rows * kHeadHeads] work items (request; head | tile << 2)
+  int32_t* ctl;            // set by launch_head: [0] item count, [1 + l] next item of layer l
 };
 
 size_t head_workspace_bytes(int64_t n_rows);

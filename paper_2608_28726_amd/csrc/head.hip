@@ -8,9 +8,12 @@
 // The tokens of all requests are processed together as rows:
 //  head_qkv_kernel   64-row tiles: (first layer: projection + encoding), the
 //                    QKV projection on MFMA (v_mfma_f32_16x16x4f32);
-//  head_attn_kernel  4 waves per (request, head, 64 queries), 16 queries
-//                    each, over all of the request's keys: scores and value
-//                    products on MFMA, online softmax per query;
+//  head_plan_kernel  one workgroup: the attention's work items (request,
+//                    head, 64 queries), the heaviest first;
+//  head_attn_kernel  persistent workgroups of 4 waves that take the items in
+//                    that order; 16 queries per wave over all of the
+//                    request's keys: scores and value products on MFMA,
+//                    online softmax per query;
 //  head_ffn_kernel   64-row tiles: output projection, residual, LayerNorm,
 //                    feed-forward (MFMA), residual, LayerNorm;
 //  head_pool_kernel  one workgroup per request: mean pool, linear, sigmoid.
@@ -225,18 +228,18 @@ constexpr int kAttnQ = 16;                      // queries per wave
 constexpr int kAttnWgQ = kAttnWaves * kAttnQ;   // queries per workgroup
 constexpr int kKT = 64;                         // keys per staged tile
 constexpr int kKPad = DH + 1;                   // LDS row of one key
+#ifndef PR_ATTN_PER_CU
+#define PR_ATTN_PER_CU 2
+#endif
+constexpr int kAttnPersist = PR_ATTN_PER_CU * 256;  // persistent attention workgroups
 typedef float fx4 __attribute__((ext_vector_type(4)));
 
-__global__ __launch_bounds__(kAttnWaves * kWave) void head_attn_kernel(HeadArgs a) {
-  __shared__ float sK[2][kKT * kKPad];
-  __shared__ float sV[2][kKT * kKPad];
-  const int64_t req = blockIdx.x;
-  const int hd = blockIdx.y;
-  const int64_t lo = a.offsets[req], hi = a.offsets[req + 1];
+// One work item: queries [q0, q0 + 64) of request [lo, hi) and head hd. Every
+// thread of the workgroup takes the same number of barriers; the LDS buffers
+// are free again when it returns.
+__device__ __forceinline__ void attend(const HeadArgs& a, int64_t lo, int64_t hi, int hd, int64_t q0,
+                                       float (&sK)[2][kKT * kKPad], float (&sV)[2][kKT * kKPad]) {
   const int64_t T = hi - lo;
-  if (T > a.max_len) return;  // scored NaN by the pool kernel
-  const int64_t q0 = lo + static_cast<int64_t>(blockIdx.z) * kAttnWgQ;
-  if (q0 >= hi) return;
   const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
   const int i16 = lane % 16, g = lane / 16;
   const int64_t qw = q0 + w * kAttnQ;  // this wave's first query
@@ -351,6 +354,90 @@ __global__ __launch_bounds__(kAttnWaves * kWave) void head_attn_kernel(HeadArgs 
   }
 }
 
+// Persistent: each workgroup takes work items in list order (the heaviest
+// first) until the list of the layer is used up, so that workgroups that
+// drew short requests take more of them. Every workgroup ends when it draws
+// an index past the item count.
+__global__ __launch_bounds__(kAttnWaves * kWave) void head_attn_kernel(HeadArgs a, int layer) {
+  __shared__ float sK[2][kKT * kKPad];
+  __shared__ float sV[2][kKT * kKPad];
+  __shared__ int32_t s_item;
+  const int32_t n_items = a.ctl[0];
+  for (;;) {
+    if (threadIdx.x == 0) s_item = atomicAdd(&a.ctl[1 + layer], 1);
+    __syncthreads();
+    const int32_t it = s_item;
+    __syncthreads();  // every thread has read s_item before the next draw
+    if (it >= n_items) return;
+    const int32_t req = a.items[2 * it];
+    const int32_t ht = a.items[2 * it + 1];
+    const int64_t lo = a.offsets[req], hi = a.offsets[req + 1];
+    attend(a, lo, hi, ht & 3, lo + static_cast<int64_t>(ht >> 2) * kAttnWgQ, sK, sV);
+  }
+}
+
+// The attention's work list: for every request of 1..max_len tokens, its
+// kHeadHeads x ceil(T / 64) items (head, 64 queries), ordered by the
+// request's number of key tiles, largest first (a counting sort over that
+// number, clamped to kPlanBins - 1), and the counters of the two layers set
+// to zero. One workgroup.
+constexpr int kPlanThreads = 1024;
+constexpr int kPlanBins = 1024;
+__global__ __launch_bounds__(kPlanThreads) void head_plan_kernel(HeadArgs a) {
+  __shared__ int32_t cnt[kPlanBins];
+  __shared__ int32_t pos[kPlanBins];
+  for (int b = threadIdx.x; b < kPlanBins; b += kPlanThreads) cnt[b] = 0;
+  __syncthreads();
+  auto tiles_of = [&](int32_t r) -> int32_t {
+    const int64_t T = static_cast<int64_t>(a.offsets[r + 1]) - a.offsets[r];
+    return (T >= 1 && T <= a.max_len) ? static_cast<int32_t>((T + kAttnWgQ - 1) / kAttnWgQ) : 0;
+  };
+  for (int32_t r = threadIdx.x; r < a.n_req; r += kPlanThreads) {
+    const int32_t nt = tiles_of(r);
+    if (nt > 0) atomicAdd(&cnt[nt < kPlanBins ? nt : kPlanBins - 1], NH * nt);
+  }
+  __syncthreads();
+  {  // starting positions, largest bin first: thread j takes bin kPlanBins - 1 - j
+    static_assert(kPlanBins == kPlanThreads, "one bin per thread");
+    __shared__ int32_t wsum[kPlanThreads / kWave];
+    const int j = threadIdx.x, lane = j % kWave, wv = j / kWave;
+    const int32_t c = cnt[kPlanBins - 1 - j];
+    int32_t x = c;  // inclusive scan within the wave
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+      const int32_t t = __shfl_up(x, d);
+      if (lane >= d) x += t;
+    }
+    if (lane == kWave - 1) wsum[wv] = x;
+    __syncthreads();
+    int32_t before = 0;
+    for (int k = 0; k < wv; ++k) before += wsum[k];
+    pos[kPlanBins - 1 - j] = before + x - c;
+    if (j == kPlanThreads - 1) {
+      // the item count; it fits the list when the offsets meet their
+      // precondition (non-decreasing, within the rows), and the list is
+      // never written past its size in any case
+      const int64_t cap = NH * a.n_rows;
+      a.ctl[0] = static_cast<int32_t>(before + x < cap ? before + x : cap);
+      for (int l = 0; l < kHeadLayers; ++l) a.ctl[1 + l] = 0;
+    }
+  }
+  __syncthreads();
+  for (int32_t r = threadIdx.x; r < a.n_req; r += kPlanThreads) {
+    const int32_t nt = tiles_of(r);
+    if (nt == 0) continue;
+    int32_t p = atomicAdd(&pos[nt < kPlanBins ? nt : kPlanBins - 1], NH * nt);
+    const int64_t cap = NH * a.n_rows;
+    for (int32_t q = 0; q < nt; ++q) {
+      for (int hd = 0; hd < NH; ++hd, ++p) {
+        if (p >= cap) continue;
+        a.items[2 * p] = r;
+        a.items[2 * p + 1] = hd | (q << 2);
+      }
+    }
+  }
+}
+
 // Output projection, residual and LayerNorm, feed-forward, residual and
 // LayerNorm of a 64-row tile.
 __global__ __launch_bounds__(kTileThreads) void head_ffn_kernel(HeadArgs a, int layer, const float* Hin,
@@ -451,8 +538,12 @@ __global__ __launch_bounds__(kPoolThreads) void head_pool_kernel(HeadArgs a, con
   }
 }
 
+// Rows of activations, then the work list (at most kHeadHeads items per row:
+// a request of T >= 1 tokens has ceil(T / 64) <= T query tiles) and the
+// counters.
 size_t head_workspace_bytes(int64_t n_rows) {
-  return static_cast<size_t>(n_rows) * (2 * D + QKV + D) * sizeof(float);
+  return static_cast<size_t>(n_rows) * ((2 * D + QKV + D) * sizeof(float) + 2 * NH * sizeof(int32_t)) +
+         static_cast<size_t>(1 + kHeadLayers) * sizeof(int32_t);
 }
 
 hipError_t launch_head(const HeadArgs& args, hipStream_t stream) {
@@ -462,10 +553,15 @@ hipError_t launch_head(const HeadArgs& args, hipStream_t stream) {
   float* H1 = H0 + a.n_rows * D;
   a.qkv = H1 + a.n_rows * D;
   a.att = a.qkv + a.n_rows * QKV;
+  a.items = reinterpret_cast<int32_t*>(a.att + a.n_rows * D);
+  a.ctl = a.items + 2 * NH * a.n_rows;
   const unsigned tiles = static_cast<unsigned>((a.n_rows + kTile - 1) / kTile);
-  const dim3 attn_grid(static_cast<unsigned>(a.n_req), NH,
-                       static_cast<unsigned>((a.max_len + kAttnWgQ - 1) / kAttnWgQ));
+  // persistent attention workgroups: two per CU of this part, fewer when
+  // there are fewer items than that
+  const int64_t max_items = NH * a.n_rows;
+  const unsigned attn_grid = static_cast<unsigned>(max_items < kAttnPersist ? max_items : kAttnPersist);
   if (a.n_rows > 0) {
+    head_plan_kernel<<<1, kPlanThreads, 0, stream>>>(a);
     float* Hin = H0;
     float* Hout = H1;
     for (int l = 0; l < kHeadLayers; ++l) {
@@ -473,7 +569,7 @@ hipError_t launch_head(const HeadArgs& args, hipStream_t stream) {
         head_qkv_kernel<true><<<tiles, kTileThreads, 0, stream>>>(a, 0, nullptr, Hin);
       else
         head_qkv_kernel<false><<<tiles, kTileThreads, 0, stream>>>(a, l, Hin, nullptr);
-      head_attn_kernel<<<attn_grid, kAttnWaves * kWave, 0, stream>>>(a);
+      head_attn_kernel<<<attn_grid, kAttnWaves * kWave, 0, stream>>>(a, l);
       head_ffn_kernel<<<tiles, kTileThreads, 0, stream>>>(a, l, Hin, Hout);
       float* t = Hin;
       Hin = Hout;
