@@ -99,3 +99,28 @@ def test_end_to_end_from_logits():
     expect = (ref >= w.tau).astype(np.uint8)
     band = np.abs(ref - w.tau) <= 1e-5
     assert np.all((ship.cpu().numpy() == expect) | band)
+
+
+def test_work_list_edges():
+    """The attention's work list: no item at all (every request empty or
+    longer than max_len), many empty requests around a few real ones, and
+    one request of 1,500 tokens (24 key tiles) among short ones; scores
+    against the oracle and bit-identical across calls."""
+    weights = wl.head_weights(seed=9)
+    X, off = synthetic_sequence([300, 0, 400], 21)
+    got = run_head(X, off, weights, max_len=200)  # no request within max_len: an empty list
+    assert np.isnan(got).all()
+    lengths = [0] * 40 + [5, 0, 70] + [0] * 20
+    X, off = synthetic_sequence(lengths, 22)
+    got = run_head(X, off, weights, max_len=70)
+    ref = ohead.head_scores(X.astype(np.float64), off, weights.astype(np.float64))
+    assert_floats("head score (empty requests)", got, ref)
+    assert np.isnan(got[[i for i, n in enumerate(lengths) if n == 0]]).all()
+    lengths = [1500, 3, 64, 65, 17]
+    X, off = synthetic_sequence(lengths, 23)
+    print(f"case head work list rows={X.shape[0]}", flush=True)
+    got = run_head(X, off, weights, max_len=1500)
+    ref = ohead.head_scores(X.astype(np.float64), off, weights.astype(np.float64))
+    assert_floats("head score (one long request)", got, ref)
+    again = run_head(X, off, weights, max_len=1500)
+    assert np.array_equal(got.view(np.uint32), again.view(np.uint32))
