@@ -16,11 +16,18 @@
 //     below 5e-5: bins are 0.018 nats wide); the prefix sums locate a window
 //     of bins whose cumulative mass brackets P of the total with a relative
 //     margin of 5e-4. (Integer LDS atomics are far cheaper than float ones);
-//  2. an exact pass: float64 sums of mass, count and entropy term over the
-//     logits above the window, the window's logits gathered into LDS, and
-//     the float64 total over every binned logit;
-//  3. a bitonic sort of the window (descending) and a float64 scan along it
-//     give the exact k; the crossing is verified to lie inside the window.
+//  2. a second pass that sums the masses above the window and in total and
+//     gathers the window's logits into LDS, in one of three forms: sparse
+//     (peaked rows: only the buckets that can reach the window are read, in
+//     float64, and the mass below the window comes from the histogram with
+//     a bound on its error); float32 (flat rows: every binned logit's mass
+//     by the hardware exp2, float64 sums, and a certified bound on the
+//     error of the test quantity); float64 over every binned logit (where
+//     neither bound decides);
+//  3. a bitonic sort of the window (descending; one wave in registers for
+//     up to 512 logits) and a float64 scan along it give k; it is taken
+//     only where the uncertainty of the sums leaves one index, and the
+//     crossing is verified to lie inside the window.
 // Logits beyond 50 nats can never be in a nucleus with P < 1 (their total
 // mass is below V * e^-50 of S). Float64 exponentials use a table-driven
 // method (Tang, ACM TOMS 15(2), 1989): exp(d) = 2^(n/64) * exp(r) with
