@@ -209,7 +209,9 @@ def test_verifier_head_rejects_bad_arguments():
     from paper_2608_28726_amd import _abi
     p = C.c_void_p(256)
     ws = int(lib.pr_verifier_head_workspace(10))
-    assert ws == 10 * (2 * 64 + 192 + 64) * 4
+    # per row: H0, H1, QKV and the attention output (float32), plus the attention's work list
+    # (at most 4 items of 2 int32 per row); then the item count and one counter per layer
+    assert ws == 10 * ((2 * 64 + 192 + 64) * 4 + 4 * 2 * 4) + (1 + 2) * 4
     assert lib.pr_verifier_head(p, 10, p, 2, 0, p, p, p, ws, None) == _abi.PR_ERR_INVALID_ARG      # max_len < 1
     assert lib.pr_verifier_head(p, -1, p, 2, 8, p, p, p, ws, None) == _abi.PR_ERR_INVALID_ARG      # n_rows < 0
     assert lib.pr_verifier_head(p, 10, None, 2, 8, p, p, p, ws, None) == _abi.PR_ERR_INVALID_ARG   # offsets
