@@ -246,14 +246,15 @@ def read_probe(torch, wl, buffers, reps=4):
     L = wl.tools()
     stream = torch.cuda.current_stream()
     best = None
-    for blocks, unroll in ((2048, 4), (4096, 4), (8192, 4), (16384, 4), (2048, 8), (4096, 8), (8192, 8),
-                           (2048, 16), (4096, 16)):
-        sink = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda")
+    shapes = ((4096, 8, 256), (8192, 8, 256), (16384, 4, 256), (16384, 8, 256), (8192, 8, 512), (16384, 4, 512),
+              (16384, 8, 512), (8192, 8, 1024), (16384, 8, 1024), (16384, 16, 1024))
+    for blocks, unroll, threads in shapes:
+        sink = torch.zeros(blocks * threads, dtype=torch.int32, device="cuda")
         nb = [(b.numel() * b.element_size()) // 16 * 16 for b in buffers]
 
         def launch(k):
             st = L.prt_read_probe(ctypes.c_void_p(buffers[k % len(buffers)].data_ptr()), nb[k % len(buffers)],
-                                  ctypes.c_void_p(sink.data_ptr()), blocks, unroll,
+                                  ctypes.c_void_p(sink.data_ptr()), blocks, unroll, threads,
                                   ctypes.c_void_p(stream.cuda_stream))
             if st != 0:
                 raise RuntimeError(f"prt_read_probe failed with status {st}")
@@ -270,9 +271,8 @@ def read_probe(torch, wl, buffers, reps=4):
         gbs = nbytes / (ms * 1e-3) / 1e9
         if best is None or gbs > best["gb_per_s"]:
             best = {"gb_per_s": gbs, "bytes_per_launch": nbytes, "ms": ms, "blocks": blocks,
-                    "loads_in_flight_per_thread": unroll,
-                    "kernel": "read_probe_kernel (nontemporal 16-byte loads, 256 threads per workgroup; "
-                              "best of 9 grid shapes)"}
+                    "threads_per_workgroup": threads, "loads_in_flight_per_thread": unroll,
+                    "kernel": f"read_probe_kernel (nontemporal 16-byte loads; best of {len(shapes)} launch shapes)"}
     return best
 
 

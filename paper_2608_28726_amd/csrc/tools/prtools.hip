@@ -119,7 +119,7 @@ typedef uint32_t vec4u __attribute__((ext_vector_type(4)));
 // is stored only if it equals a value no real data produces, so the loads
 // cannot be dropped and nothing is written in practice.
 template <int UNROLL>
-__global__ void __launch_bounds__(256) read_probe_kernel(const vec4u* __restrict__ p, int64_t n_vec,
+__global__ void __launch_bounds__(1024) read_probe_kernel(const vec4u* __restrict__ p, int64_t n_vec,
                                                          uint32_t* __restrict__ sink) {
   const int64_t gid = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   const int64_t step = static_cast<int64_t>(gridDim.x) * blockDim.x;
@@ -209,21 +209,24 @@ int prt_fill_logits(void* out, int dtype, int64_t n_rows, int32_t V, int64_t row
 }
 
 // Launches the read probe over nbytes (a multiple of 16) at buf (16-byte
-// aligned) with `blocks` workgroups of 256 threads and `unroll` (4, 8 or 16)
-// loads in flight per thread. sink is a device array of blocks * 256 uint32
-// that is written only in the case described above.
-int prt_read_probe(const void* buf, int64_t nbytes, uint32_t* sink, int32_t blocks, int32_t unroll, void* stream) {
+// aligned) with `blocks` workgroups of `threads` (256, 512 or 1024) threads
+// and `unroll` (4, 8 or 16) loads in flight per thread. sink is a device
+// array of blocks * threads uint32 that is written only in the case
+// described above.
+int prt_read_probe(const void* buf, int64_t nbytes, uint32_t* sink, int32_t blocks, int32_t unroll, int32_t threads,
+                   void* stream) {
   if (!buf || !sink || nbytes <= 0 || nbytes % 16 != 0 || blocks <= 0) return 1;
+  if (threads != 256 && threads != 512 && threads != 1024) return 1;
   if (reinterpret_cast<uintptr_t>(buf) % 16 != 0) return 1;
   const vec4u* p = static_cast<const vec4u*>(buf);
   hipStream_t st = static_cast<hipStream_t>(stream);
   const dim3 grid(static_cast<unsigned>(blocks));
   if (unroll == 4)
-    hipLaunchKernelGGL(read_probe_kernel<4>, grid, dim3(256), 0, st, p, nbytes / 16, sink);
+    hipLaunchKernelGGL(read_probe_kernel<4>, grid, dim3(threads), 0, st, p, nbytes / 16, sink);
   else if (unroll == 8)
-    hipLaunchKernelGGL(read_probe_kernel<8>, grid, dim3(256), 0, st, p, nbytes / 16, sink);
+    hipLaunchKernelGGL(read_probe_kernel<8>, grid, dim3(threads), 0, st, p, nbytes / 16, sink);
   else if (unroll == 16)
-    hipLaunchKernelGGL(read_probe_kernel<16>, grid, dim3(256), 0, st, p, nbytes / 16, sink);
+    hipLaunchKernelGGL(read_probe_kernel<16>, grid, dim3(threads), 0, st, p, nbytes / 16, sink);
   else
     return 1;
   return hipGetLastError() == hipSuccess ? 0 : 3;

@@ -269,7 +269,7 @@ def tools():
         L.prt_fill_logits.argtypes = [vp, ctypes.c_int, i64, i32, i64, ctypes.c_uint64, i64, vp, vp, vp, vp, vp,
                                       vp, vp]
         L.prt_fill_logits.restype = ctypes.c_int
-        L.prt_read_probe.argtypes = [vp, i64, vp, i32, i32, vp]
+        L.prt_read_probe.argtypes = [vp, i64, vp, i32, i32, i32, vp]
         L.prt_read_probe.restype = ctypes.c_int
         L.prt_exp2_max_rel_err.argtypes = [ctypes.c_float, ctypes.c_float, vp, vp]
         L.prt_exp2_max_rel_err.restype = ctypes.c_int
