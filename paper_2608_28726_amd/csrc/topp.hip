@@ -27,7 +27,10 @@
 //  3. a bitonic sort of the window (descending; one wave in registers for
 //     up to 512 logits) and a float64 scan along it give k; it is taken
 //     only where the uncertainty of the sums leaves one index, and the
-//     crossing is verified to lie inside the window.
+//     crossing is verified to lie inside the window. A larger window is
+//     first split into 256 sub-buckets of its values with fixed-point sums
+//     (integer atomics), and only the sub-buckets the crossing can fall in
+//     are sorted.
 // Logits beyond 50 nats can never be in a nucleus with P < 1 (their total
 // mass is below V * e^-50 of S). Float64 exponentials use a table-driven
 // method (Tang, ACM TOMS 15(2), 1989): exp(d) = 2^(n/64) * exp(r) with
@@ -59,6 +62,7 @@ constexpr int kBins = 4096;     // fallback histogram: bins over kDMax nats belo
 constexpr float kDMax = 50.0f;  // nats below the maximum
 constexpr int kCap = 4096;      // gathered logits sorted in LDS
 constexpr int kNW = kTpBlock / kWave;
+constexpr int kSub = 256;  // sub-buckets of a window of more than 512 logits
 constexpr int kHB = 4096;         // histogram bins of the stats pass
 constexpr float kHAbove = 25.0f;  // nats above the anchor covered by the bins
 constexpr float kHSpan = 75.0f;   // nats covered: [-kHAbove, kDMax)
@@ -99,6 +103,7 @@ struct TpShared {
   double exptab[64];  // 2^(j/64)
   double red_d[2][kNW];
   uint32_t red_u[kNW];
+  uint32_t red_m[2][kNW];
   float red_f[kNW];
   float topk[topk::kMaxK];  // the row's K largest logits (sequence variant)
   double S64, target, massAbove, Eabove, SN, EN;
@@ -107,10 +112,24 @@ struct TpShared {
   int32_t active;
   Partial p;
   uint32_t fix;
-  // radix refinement
-  double rmass[256], rE[256];
-  uint32_t rcnt[256];
+  // per digit of the three-pass method's radix refinement, or per
+  // sub-bucket of a large window's cut (never in use at the same time)
+  union {
+    struct {
+      double mass[256], E[256];
+      uint32_t cnt[256];
+    } rx;
+    struct {
+      unsigned long long q[kSub];   // masses, fixed point
+      unsigned long long qe[kSub];  // entropy terms, fixed point (two's complement)
+      uint32_t cnt[kSub];
+    } sb;
+  } r;
   uint32_t prefix, rdigit;
+  struct {
+    double m, e, t_lo, t_hi;  // above the crossing sub-buckets; the widened thresholds
+    uint32_t c, s_first, s_last;
+  } sc;
 };
 
 // Calls fn(z) for every logit of the row (order irrelevant), with the
@@ -166,6 +185,28 @@ __device__ __forceinline__ uint32_t block_sum_u(uint32_t v, TpShared& sh) {
   for (int k = 0; k < kNW; ++k) tot += sh.red_u[k];
   __syncthreads();
   return tot;
+}
+
+// Block-wide maxima of (a, b); every thread gets them.
+__device__ __forceinline__ void block_max2_u(uint32_t& a, uint32_t& b, TpShared& sh) {
+#pragma unroll
+  for (int o = kWave / 2; o > 0; o >>= 1) {
+    a = max(a, static_cast<uint32_t>(__shfl_xor(static_cast<int>(a), o)));
+    b = max(b, static_cast<uint32_t>(__shfl_xor(static_cast<int>(b), o)));
+  }
+  __syncthreads();
+  if (threadIdx.x % kWave == 0) {
+    sh.red_m[0][threadIdx.x / kWave] = a;
+    sh.red_m[1][threadIdx.x / kWave] = b;
+  }
+  __syncthreads();
+  a = 0u;
+  b = 0u;
+  for (int k = 0; k < kNW; ++k) {
+    a = max(a, sh.red_m[0][k]);
+    b = max(b, sh.red_m[1][k]);
+  }
+  __syncthreads();
 }
 
 // Exclusive block scan of one double per thread (thread order).
@@ -303,9 +344,9 @@ __device__ Nucleus radix_boundary(const void* row, int32_t V, int64_t h, int64_t
   for (int pass = 0; pass < 4; ++pass) {
     const int shift = 24 - 8 * pass;
     for (int b = threadIdx.x; b < 256; b += kTpBlock) {
-      sh.rmass[b] = 0.0;
-      sh.rE[b] = 0.0;
-      sh.rcnt[b] = 0;
+      sh.r.rx.mass[b] = 0.0;
+      sh.r.rx.E[b] = 0.0;
+      sh.r.rx.cnt[b] = 0;
     }
     __syncthreads();
     for_each_logit<Tin>(row, V, h, nvec, [&](float z) {
@@ -318,24 +359,24 @@ __device__ Nucleus radix_boundary(const void* row, int32_t V, int64_t h, int64_t
       const uint32_t dg = (key >> shift) & 255u;
       const double dd = D.d64(z);
       const double e = exp(dd);
-      atomicAdd(&sh.rmass[dg], e);
-      atomicAdd(&sh.rE[dg], e * dd);
-      atomicAdd(&sh.rcnt[dg], 1u);
+      atomicAdd(&sh.r.rx.mass[dg], e);
+      atomicAdd(&sh.r.rx.E[dg], e * dd);
+      atomicAdd(&sh.r.rx.cnt[dg], 1u);
     });
     __syncthreads();
     if (threadIdx.x == 0) {
       int dg = 255;
       for (; dg > 0; --dg) {  // descending keys: larger logits first
-        if (massGT + sh.rmass[dg] >= sh.target) break;
-        massGT += sh.rmass[dg];
-        EGT += sh.rE[dg];
-        cntGT += sh.rcnt[dg];
+        if (massGT + sh.r.rx.mass[dg] >= sh.target) break;
+        massGT += sh.r.rx.mass[dg];
+        EGT += sh.r.rx.E[dg];
+        cntGT += sh.r.rx.cnt[dg];
       }
       sh.rdigit = static_cast<uint32_t>(dg);
       sh.massAbove = massGT;
       sh.Eabove = EGT;
       sh.cntAbove = cntGT;
-      sh.rcount = sh.rcnt[dg];
+      sh.rcount = sh.r.rx.cnt[dg];
     }
     __syncthreads();
     prefix |= sh.rdigit << shift;
@@ -720,22 +761,12 @@ __device__ __forceinline__ bool cut_window_wave(TpShared& sh, int nw, uint32_t c
   return true;
 }
 
-// Step 3 of the histogram method: the window's nw_all logits (in sh.win)
-// sorted into descending order and scanned. A logit's mass is exp(dd(z)) in
-// the caller's frame; mA and eA are the mass and the entropy sum (nats of
-// that frame) above the window, cA the number of logits there. The cutoff
-// is the first index j at which the running mass mA + C_j reaches the
-// target; thr(wm, t_lo, t_hi) gives the interval [t_lo, t_hi] the target
-// may lie in (wm: the window's total mass), and j is taken only where both
-// ends give the same index. Returns false when they do not, or when the
-// crossing lies outside the window; else the nucleus size and its mass and
-// entropy sums in the caller's frame.
+// cut_window for any window of at most kCap logits: a workgroup-wide
+// bitonic sort, then block scans.
 template <typename DD, typename Thr>
-__device__ bool cut_window(TpShared& sh, uint32_t nw_all, uint32_t cA, double mA, double eA, DD dd_of, Thr thr,
-                           Nucleus& nuc) {
+__device__ bool cut_window_block(TpShared& sh, int nw, uint32_t cA, double mA, double eA, DD dd_of, Thr thr,
+                                 Nucleus& nuc) {
   const double* tab = sh.exptab;
-  const int nw = static_cast<int>(nw_all);
-  if (nw <= 512) return cut_window_wave(sh, nw, cA, mA, eA, dd_of, thr, nuc);
   int n2 = 2;
   while (n2 < nw) n2 <<= 1;
   for (int i = nw + threadIdx.x; i < n2; i += kTpBlock) sh.win[i] = -INFINITY;
@@ -795,6 +826,170 @@ __device__ bool cut_window(TpShared& sh, uint32_t nw_all, uint32_t cA, double mA
   nuc.S = sh.SN;
   nuc.E = sh.EN;
   return true;
+}
+
+__device__ __forceinline__ float key_float(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
+}
+
+// cut_window for a window of more than 512 logits. Its logits fall into kSub
+// sub-buckets by their order-preserving keys (sub-bucket 0 holds the largest
+// values; equal values share one), and each sub-bucket sums its count, masses
+// and entropy terms in 64-bit fixed point with integer atomics, so that the
+// sums do not depend on the order of the additions. The sub-buckets before
+// the first one whose running mass can reach the target lie above the cutoff
+// whole; the logits of the sub-buckets in which the crossing can fall move to
+// the front of sh.win and are cut alone, from the mass, entropy sum and count
+// above them. A fixed-point mass errs by less than one unit (mref 2^-48), so
+// the target interval is widened by twice the error of those sums: a cutoff
+// taken inside the wider interval is the cutoff of the narrower one.
+template <typename DD, typename Thr>
+__device__ __forceinline__ bool cut_window_sub(TpShared& sh, int nw, uint32_t cA, double mA, double eA, DD dd_of,
+                                               Thr thr, Nucleus& nuc) {
+  constexpr int kPer = kCap / kTpBlock;
+  constexpr uint32_t kNone = 0xffffffffu;
+  const double* tab = sh.exptab;
+  float z[kPer];
+  uint32_t key[kPer];
+  uint32_t kmax = 0u, knmin = 0u;  // largest key, largest complemented key
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int i = static_cast<int>(threadIdx.x) + k * kTpBlock;
+    z[k] = i < nw ? sh.win[i] : 0.0f;
+    key[k] = float_key(z[k]);
+    if (i < nw) {
+      kmax = max(kmax, key[k]);
+      knmin = max(knmin, ~key[k]);
+    }
+  }
+  if (threadIdx.x < kSub) {
+    sh.r.sb.q[threadIdx.x] = 0ull;
+    sh.r.sb.qe[threadIdx.x] = 0ull;
+    sh.r.sb.cnt[threadIdx.x] = 0u;
+  }
+  block_max2_u(kmax, knmin, sh);  // its barriers also order the clearing before the sums
+  const uint32_t hi = kmax, span = kmax - ~knmin;
+  const int shift = span < static_cast<uint32_t>(kSub) ? 0 : 24 - __clz(static_cast<int>(span));  // span >> shift < kSub
+  const double dd_hi = dd_of(key_float(hi)), dd_lo = dd_of(key_float(~knmin));
+  const double mref = exp_tang(dd_hi, tab) * (1.0 + 0x1p-30);  // at least every mass of the window
+  if (!(mref > 0x1p-900 && mref < 0x1p900)) return cut_window_block(sh, nw, cA, mA, eA, dd_of, thr, nuc);
+  const double scale = 0x1p48 / mref;
+  const double scale_e = 0x1p48 / (mref * fmax(fmax(fabs(dd_hi), fabs(dd_lo)), 1.0));
+  int sb[kPer];
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int i = static_cast<int>(threadIdx.x) + k * kTpBlock;
+    sb[k] = static_cast<int>((hi - key[k]) >> shift);
+    if (i < nw) {
+      const double dd = dd_of(z[k]);
+      const double e = exp_tang(dd, tab);
+      atomicAdd(&sh.r.sb.q[sb[k]], static_cast<unsigned long long>(e * scale));
+      atomicAdd(&sh.r.sb.qe[sb[k]], static_cast<unsigned long long>(static_cast<long long>(e * dd * scale_e)));
+      atomicAdd(&sh.r.sb.cnt[sb[k]], 1u);
+    }
+  }
+  __syncthreads();
+  if (threadIdx.x < kWave) {
+    // wave 0: kSub / 64 consecutive sub-buckets per lane, scanned in order
+    constexpr int kPL = kSub / kWave;
+    const int lane = static_cast<int>(threadIdx.x);
+    double m[kPL], ee[kPL], c[kPL];
+    double lm = 0.0, le = 0.0, lc = 0.0;
+#pragma unroll
+    for (int j = 0; j < kPL; ++j) {
+      const int s = kPL * lane + j;
+      m[j] = static_cast<double>(sh.r.sb.q[s]) / scale;
+      ee[j] = static_cast<double>(static_cast<long long>(sh.r.sb.qe[s])) / scale_e;
+      c[j] = static_cast<double>(sh.r.sb.cnt[s]);
+      lm += m[j];
+      le += ee[j];
+      lc += c[j];
+    }
+    const double ism = wave_incl_scan_d(lm), ise = wave_incl_scan_d(le), isc = wave_incl_scan_d(lc);
+    const double pm = __shfl_up(ism, 1), pe = __shfl_up(ise, 1), pc = __shfl_up(isc, 1);
+    const double wm = __shfl(ism, kWave - 1);
+    double t_lo, t_hi;
+    thr(wm, t_lo, t_hi);
+    // each fixed-point mass is low by less than 1 / scale; the conversions and
+    // the float64 sums add a few units in the last place
+    const double err = (static_cast<double>(nw) + 8.0) / scale + 1e-14 * (fabs(mA) + wm);
+    t_lo -= 2.0 * err;
+    t_hi += 2.0 * err;
+    const bool inside = mA < t_lo && !(mA + wm < t_hi);
+    int slo = kSub, shi = kSub;
+    double run = mA + (lane > 0 ? pm : 0.0);
+#pragma unroll
+    for (int j = 0; j < kPL; ++j) {
+      run += m[j];
+      if (slo == kSub && run >= t_lo) slo = kPL * lane + j;
+      if (shi == kSub && run >= t_hi) shi = kPL * lane + j;
+    }
+    const uint64_t mlo = __ballot(slo < kSub), mhi = __ballot(shi < kSub);
+    const int sf = mlo ? __shfl(slo, static_cast<int>(__builtin_ctzll(mlo))) : kSub;
+    const int sl = mhi ? __shfl(shi, static_cast<int>(__builtin_ctzll(mhi))) : kSub;
+    const bool ok = inside && sf < kSub && sl < kSub;
+    if (ok && sf / kPL == lane) {  // the sums over the sub-buckets before sf
+      double bm = mA + (lane > 0 ? pm : 0.0), be = eA + (lane > 0 ? pe : 0.0), bc = lane > 0 ? pc : 0.0;
+#pragma unroll
+      for (int j = 0; j < kPL; ++j) {
+        if (j < sf % kPL) {
+          bm += m[j];
+          be += ee[j];
+          bc += c[j];
+        }
+      }
+      sh.sc.m = bm;
+      sh.sc.e = be;
+      sh.sc.c = cA + static_cast<uint32_t>(bc);
+    }
+    if (lane == 0) {
+      sh.sc.t_lo = t_lo;
+      sh.sc.t_hi = t_hi;
+      sh.sc.s_first = ok ? static_cast<uint32_t>(sf) : kNone;
+      sh.sc.s_last = static_cast<uint32_t>(sl);
+      sh.wcount = 0u;
+    }
+  }
+  __syncthreads();
+  const uint32_t sf = sh.sc.s_first, sl = sh.sc.s_last;
+  if (sf == kNone) return false;
+  // every thread holds its logits in registers: the window can be rewritten
+#pragma unroll
+  for (int k = 0; k < kPer; ++k) {
+    const int i = static_cast<int>(threadIdx.x) + k * kTpBlock;
+    if (i < nw && static_cast<uint32_t>(sb[k]) >= sf && static_cast<uint32_t>(sb[k]) <= sl) {
+      const uint32_t slot = atomicAdd(&sh.wcount, 1u);
+      sh.win[slot] = z[k];
+    }
+  }
+  __syncthreads();
+  const int nc = static_cast<int>(sh.wcount);
+  const double t_lo = sh.sc.t_lo, t_hi = sh.sc.t_hi, bm = sh.sc.m, be = sh.sc.e;
+  const uint32_t bc = sh.sc.c;
+  auto thr_c = [&](double, double& lo, double& hi_) {
+    lo = t_lo;
+    hi_ = t_hi;
+  };
+  if (nc <= 512) return cut_window_wave(sh, nc, bc, bm, be, dd_of, thr_c, nuc);
+  return cut_window_block(sh, nc, bc, bm, be, dd_of, thr_c, nuc);
+}
+
+// Step 3 of the histogram method: the window's nw_all logits (in sh.win)
+// sorted into descending order and scanned. A logit's mass is exp(dd(z)) in
+// the caller's frame; mA and eA are the mass and the entropy sum (nats of
+// that frame) above the window, cA the number of logits there. The cutoff
+// is the first index j at which the running mass mA + C_j reaches the
+// target; thr(wm, t_lo, t_hi) gives the interval [t_lo, t_hi] the target
+// may lie in (wm: the window's total mass), and j is taken only where both
+// ends give the same index. Returns false when they do not, or when the
+// crossing lies outside the window; else the nucleus size and its mass and
+// entropy sums in the caller's frame.
+template <typename DD, typename Thr>
+__device__ bool cut_window(TpShared& sh, uint32_t nw_all, uint32_t cA, double mA, double eA, DD dd_of, Thr thr,
+                           Nucleus& nuc) {
+  const int nw = static_cast<int>(nw_all);
+  if (nw <= 512) return cut_window_wave(sh, nw, cA, mA, eA, dd_of, thr, nuc);
+  return cut_window_sub(sh, nw, cA, mA, eA, dd_of, thr, nuc);
 }
 
 // Steps 2 and 3 of the histogram method: the exact pass over the row (dense)

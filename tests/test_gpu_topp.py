@@ -187,6 +187,45 @@ def test_topp_flat_rows(dtype):
     compare_features(gpu_features(logits, ids, T, P), oracle_features(logits, ids, T, P))
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_topp_large_windows(dtype):
+    """Windows of 513 to 4,096 logits, cut through their sub-buckets: a
+    plateau of distinct values, a tie group of 1,500 at the crossing (its
+    sub-bucket alone holds more than 512 logits and takes the workgroup
+    sort), a window spanning fewer than 256 float steps (one value per
+    sub-bucket), and one crossing zero (keys of both signs)."""
+    V = 65536
+    rng = np.random.default_rng(4096)
+    rows, ids, Ps = [], [], []
+    def add(z, P):
+        pos = np.flatnonzero(z > -10)
+        rows.append(z); ids.append(int(pos[len(pos) // 2])); Ps.append(P)
+    for n, P in ((600, 0.6), (1500, 0.7), (3000, 0.8), (4000, 0.9)):
+        z = np.full(V, -20.0)
+        z[rng.choice(V, n, replace=False)] = rng.uniform(0.0, 1e-3, n)
+        add(z, P)                                           # plateau of n distinct values
+    z = np.full(V, -20.0)
+    pos = rng.choice(V, 3000, replace=False)
+    z[pos[:1500]] = 0.5
+    z[pos[1500:]] = rng.uniform(0.49, 0.51, 1500)
+    add(z, 0.5)                                             # 1,500 ties at the crossing
+    z = np.full(V, -20.0)
+    k = np.repeat(np.arange(200), 10)
+    z[rng.choice(V, k.size, replace=False)] = 1.0 + k * 2.0 ** -23
+    add(z, 0.6)                                             # 200 values one float step apart, 10 of each
+    z = np.full(V, -20.0)
+    z[rng.choice(V, 2500, replace=False)] = rng.uniform(-1e-3, 1e-3, 2500)
+    add(z, 0.8)                                             # window across zero
+    n = len(rows)
+    logits, ids, T, P = _run(np.stack(rows), ids, np.ones(n), Ps, dtype)
+    print(f"case topp large windows {dtype}", flush=True)
+    g = gpu_features(logits, ids, T, P)
+    compare_features(g, oracle_features(logits, ids, T, P))
+    g2 = gpu_features(logits, ids, T, P)
+    for key in g:
+        assert np.array_equal(g[key].view(np.uint32), g2[key].view(np.uint32)), key
+
+
 def test_hardware_exp2_bound():
     """The float32 pass of the top-p kernel certifies its masses with a bound
     of 1e-7 on the relative error of the hardware exp2 (the constant
