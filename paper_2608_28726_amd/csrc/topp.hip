@@ -283,7 +283,9 @@ struct HistHook {
   float kz4, k04;  // the same scaled by kOffQ
   __device__ __forceinline__ void count(float z) {
     const float x = fmaf(z, kz4, k04);
-    if (x >= 0.0f && x < static_cast<float>(kHB) * kOffQ) {
+    // 0 <= x < kHB kOffQ as one unsigned compare of the bits: x is never -0
+    // (k04 is not -0), and NaN and the infinities compare above the bound
+    if (__float_as_uint(x) < __float_as_uint(static_cast<float>(kHB) * kOffQ)) {
       const uint32_t xi = static_cast<uint32_t>(x);
       atomicAdd(&bins[xi >> kOffBits], (uint64_t{1} << kCountShift) | (xi & ((1u << kOffBits) - 1)));
     }
@@ -1121,12 +1123,12 @@ __device__ __forceinline__ bool approx_cut(const void* row, int32_t V, int64_t h
     const float t = fmaf(z, c_lo, fmaf(z, c_hi, nMc));
     const float e = __builtin_amdgcn_exp2f(t);
     const double e64 = static_cast<double>(e);
-    const double et = e64 * static_cast<double>(t);  // exact
+    const double t64 = static_cast<double>(t);
     sT += e64;
-    tT += et;
+    tT = fma(e64, t64, tT);  // the product is exact: one rounding either way
     if (x < xa) {
       mA += e64;
-      tA += et;
+      tA = fma(e64, t64, tA);
     } else if (x < xb) {
       const uint32_t slot = atomicAdd(&sh.wcount, 1u);
       if (slot < static_cast<uint32_t>(kCap)) sh.win[slot] = z;
