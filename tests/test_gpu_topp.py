@@ -226,6 +226,19 @@ def test_topp_large_windows(dtype):
         assert np.array_equal(g[key].view(np.uint32), g2[key].view(np.uint32)), key
 
 
+def test_topp_large_vocabulary():
+    """A vocabulary of 2^20 + 3 (four times the largest workload's): random,
+    flat and peaked rows against the oracle's exact cutoff."""
+    V = (1 << 20) + 3
+    rng = np.random.default_rng(20)
+    rows = [rng.normal(0, 2, V), rng.normal(0, 0.01, V), rng.normal(0, 1, V)]
+    rows[2][12345] = 40.0
+    ids = [int(rng.integers(0, V)), 7, 12345]
+    logits, ids, T, P = _run(np.stack(rows), ids, [0.8, 1.2, 1.0], [0.9, 0.93, 0.5])
+    print("case topp V = 2^20 + 3", flush=True)
+    compare_features(gpu_features(logits, ids, T, P), oracle_features(logits, ids, T, P))
+
+
 def test_hardware_exp2_bound():
     """The float32 pass of the top-p kernel certifies its masses with a bound
     of 1e-7 on the relative error of the hardware exp2 (the constant
