@@ -94,7 +94,7 @@ struct TpShared {
       // summed positions inside the bin (low 40 bits: each logit adds
       // floor((offset + 1/2) * kOffQ) in [0, kOffQ), so the field stays
       // below 2^40 while V < 2^24)
-      uint64_t bins[kHB];
+      uint64_t bins[kHB + 1];  // bins[kHB] takes the logits outside them (never read)
     } hs;
     double wtab[kHB];  // exact pass: exp of each bin centre's distance from M
   } u;
@@ -283,12 +283,12 @@ struct HistHook {
   float kz4, k04;  // the same scaled by kOffQ
   __device__ __forceinline__ void count(float z) {
     const float x = fmaf(z, kz4, k04);
-    // 0 <= x < kHB kOffQ as one unsigned compare of the bits: x is never -0
-    // (k04 is not -0), and NaN and the infinities compare above the bound
-    if (__float_as_uint(x) < __float_as_uint(static_cast<float>(kHB) * kOffQ)) {
-      const uint32_t xi = static_cast<uint32_t>(x);
-      atomicAdd(&bins[xi >> kOffBits], (uint64_t{1} << kCountShift) | (xi & ((1u << kOffBits) - 1)));
-    }
+    // Without a branch: the bits of x capped at those of kHB kOffQ (x is never
+    // -0, since k04 is not; negative x, NaN and the infinities compare above
+    // the cap) send every logit outside [0, kHB kOffQ) to bins[kHB].
+    const uint32_t u = min(__float_as_uint(x), __float_as_uint(static_cast<float>(kHB) * kOffQ));
+    const uint32_t xi = static_cast<uint32_t>(__uint_as_float(u));
+    atomicAdd(&bins[xi >> kOffBits], (uint64_t{1} << kCountShift) | (xi & ((1u << kOffBits) - 1)));
   }
   template <int N>
   __device__ __forceinline__ void step(const float (&z)[N], const float (&)[N], float cmax, int64_t, const Lane&) {
