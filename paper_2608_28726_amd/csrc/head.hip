@@ -167,25 +167,40 @@ __global__ __launch_bounds__(kTileThreads) void head_qkv_kernel(HeadArgs a, int 
       sPos[threadIdx.x] = pos;
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < kTile * D; i += kTileThreads) {
-      const int rr = i / D, j = i % D;
+    // A thread keeps one feature pair (2p, 2p + 1) of its rows: the sine and
+    // the cosine of (t - 1) f_p, f_p = 10000^(-2p / 64). The angle is formed
+    // and reduced to [-pi, pi] in float64 (positions reach 10^3), its sine
+    // and cosine taken together in float32.
+    constexpr int kPairs = D / 2;
+    static_assert(kTileThreads % kPairs == 0, "a thread's pair is the same in every row");
+    const int j0 = 2 * (threadIdx.x % kPairs);
+    const double freq = exp2(-static_cast<double>(j0) / D * 13.287712379549449);
+    const float* w0 = a.weights + kW_in + j0 * 4;
+    const float* w1 = w0 + 4;
+    for (int i = threadIdx.x; i < kTile * kPairs; i += kTileThreads) {
+      const int rr = i / kPairs;
       const int64_t r = r0 + rr;
-      float h = 0.0f;
+      float h0 = 0.0f, h1 = 0.0f;
       if (r < a.n_rows) {
         const float* x = a.X + r * 4;
-        const float* w = a.weights + kW_in + j * 4;
-        h = a.weights[kB_in + j];
-        h = fmaf(w[0], x[0], h);
-        h = fmaf(w[1], x[1], h);
-        h = fmaf(w[2], x[2], h);
-        h = fmaf(w[3], x[3], h);
-        // sinusoid of position t - 1 (angles in float64: positions reach 10^3)
-        const int i2 = j & ~1;
-        const double angle = static_cast<double>(sPos[rr]) * exp2(-static_cast<double>(i2) / D * 13.287712379549449);
-        h += static_cast<float>((j & 1) ? cos(angle) : sin(angle));
-        Hout[r * D + j] = h;
+        h0 = a.weights[kB_in + j0];
+        h1 = a.weights[kB_in + j0 + 1];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          h0 = fmaf(w0[c], x[c], h0);
+          h1 = fmaf(w1[c], x[c], h1);
+        }
+        const double angle = static_cast<double>(sPos[rr]) * freq;
+        const double red = fma(-rint(angle * 0.15915494309189535), 6.283185307179586, angle);
+        float sn, cs;
+        sincosf(static_cast<float>(red), &sn, &cs);
+        h0 += sn;
+        h1 += cs;
+        Hout[r * D + j0] = h0;
+        Hout[r * D + j0 + 1] = h1;
       }
-      sA[rr * kSA + j] = h;
+      sA[rr * kSA + j0] = h0;
+      sA[rr * kSA + j0 + 1] = h1;
     }
   } else {
     stage_rows(sA, Hin, r0, a.n_rows);
