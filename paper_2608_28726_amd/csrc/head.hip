@@ -539,6 +539,9 @@ __global__ __launch_bounds__(kPoolThreads) void head_pool_kernel(HeadArgs a, con
   const int64_t T = hi - lo;
   const int c = threadIdx.x % D, p = threadIdx.x / D;
   float s = 0.0f;
+  // unrolled, so that a thread's loads are in flight together (the sum keeps
+  // its order)
+#pragma unroll 8
   for (int64_t r = lo + p; r < hi; r += kPoolThreads / D) s += H[r * D + c];
   part[p][c] = s;
   __syncthreads();
