@@ -654,29 +654,30 @@ __device__ __forceinline__ double wave_incl_scan_d(double x) {
   return x;
 }
 
-// Sorts the 512 floats a wave holds, 8 per lane (element 8 lane + k), into
+// Sorts the 64 E floats a wave holds, E per lane (element E lane + k), into
 // descending order with the same bitonic network as bitonic_desc: strides
-// below 8 compare registers of one lane, longer ones the same register of
-// lane ^ (stride / 8).
-__device__ __forceinline__ void wave_bitonic_desc512(float (&v)[8]) {
+// below E compare registers of one lane, longer ones the same register of
+// lane ^ (stride / E).
+template <int E>
+__device__ __forceinline__ void wave_bitonic_desc(float (&v)[E]) {
   const int lane = static_cast<int>(threadIdx.x % kWave);
 #pragma unroll
-  for (int size = 2; size <= 512; size <<= 1) {
+  for (int size = 2; size <= kWave * E; size <<= 1) {
 #pragma unroll
     for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      if (stride >= 8) {
+      if (stride >= E) {
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          const int i = 8 * lane + k;
-          const float p = __shfl_xor(v[k], stride >> 3);
+        for (int k = 0; k < E; ++k) {
+          const int i = E * lane + k;
+          const float p = __shfl_xor(v[k], stride / E);
           const bool keep_max = ((i & size) == 0) == ((i & stride) == 0);
           v[k] = keep_max ? fmaxf(v[k], p) : fminf(v[k], p);
         }
       } else {
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
+        for (int k = 0; k < E; ++k) {
           if (k & stride) continue;
-          const bool desc = ((8 * lane + k) & size) == 0;
+          const bool desc = ((E * lane + k) & size) == 0;
           const float a = v[k], b = v[k | stride];
           v[k] = desc ? fmaxf(a, b) : fminf(a, b);
           v[k | stride] = desc ? fminf(a, b) : fmaxf(a, b);
@@ -686,27 +687,27 @@ __device__ __forceinline__ void wave_bitonic_desc512(float (&v)[8]) {
   }
 }
 
-// cut_window for a window of at most 512 logits: wave 0 holds it in
-// registers, sorts it, forms each mass once and scans with wave prefix sums
-// (no workgroup barrier until the result is published). Same result as the
-// workgroup-wide version up to the order of float64 additions.
-template <typename DD, typename Thr>
+// cut_window for a window of at most 64 E logits: wave 0 holds it in
+// registers, E per lane, sorts it, forms each mass once and scans with wave
+// prefix sums (no workgroup barrier until the result is published). Same
+// result as the workgroup-wide version up to the order of float64 additions.
+template <int E, typename DD, typename Thr>
 __device__ __forceinline__ bool cut_window_wave(TpShared& sh, int nw, uint32_t cA, double mA, double eA, DD dd_of,
                                                 Thr thr, Nucleus& nuc) {
   const double* tab = sh.exptab;
   if (threadIdx.x < kWave) {
     const int lane = static_cast<int>(threadIdx.x);
-    float v[8];
+    float v[E];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = 8 * lane + k < nw ? sh.win[8 * lane + k] : -INFINITY;
-    wave_bitonic_desc512(v);
-    double e[8], ed[8];
+    for (int k = 0; k < E; ++k) v[k] = E * lane + k < nw ? sh.win[E * lane + k] : -INFINITY;
+    wave_bitonic_desc<E>(v);
+    double e[E], ed[E];
     double ls = 0.0, le = 0.0;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+    for (int k = 0; k < E; ++k) {
       e[k] = 0.0;
       ed[k] = 0.0;
-      if (8 * lane + k < nw) {  // the window's logits lead the sorted order (the padding is -inf)
+      if (E * lane + k < nw) {  // the window's logits lead the sorted order (the padding is -inf)
         const double dd = dd_of(v[k]);
         e[k] = exp_tang(dd, tab);
         ed[k] = e[k] * dd;
@@ -729,10 +730,10 @@ __device__ __forceinline__ bool cut_window_wave(TpShared& sh, int nw, uint32_t c
     if (inside) {
       double run = mA + cm;
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
+      for (int k = 0; k < E; ++k) {
         run += e[k];
-        if (jlo == kNone && run >= t_lo) jlo = 8 * lane + k;
-        if (jhi == kNone && run >= t_hi) jhi = 8 * lane + k;
+        if (jlo == kNone && run >= t_lo) jlo = E * lane + k;
+        if (jhi == kNone && run >= t_hi) jhi = E * lane + k;
       }
     }
     // indices grow with the lane: the first lane that has one holds the smallest
@@ -740,11 +741,11 @@ __device__ __forceinline__ bool cut_window_wave(TpShared& sh, int nw, uint32_t c
     const int jf = mlo ? __shfl(jlo, static_cast<int>(__builtin_ctzll(mlo))) : kNone;
     const int jr = mhi ? __shfl(jhi, static_cast<int>(__builtin_ctzll(mhi))) : kNone;
     const bool decided = inside && jf != kNone && jf == jr;
-    if (decided && jf / 8 == lane) {
+    if (decided && jf / E == lane) {
       double m2 = mA + cm, e2 = eA + ce;
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        if (k <= jf % 8) {
+      for (int k = 0; k < E; ++k) {
+        if (k <= jf % E) {
           m2 += e[k];
           e2 += ed[k];
         }
@@ -761,6 +762,17 @@ __device__ __forceinline__ bool cut_window_wave(TpShared& sh, int nw, uint32_t c
   nuc.S = sh.SN;
   nuc.E = sh.EN;
   return true;
+}
+
+// cut_window for a window of at most 512 logits: the one-wave cut with the
+// fewest logits per lane that holds it.
+template <typename DD, typename Thr>
+__device__ __forceinline__ bool cut_window_small(TpShared& sh, int nw, uint32_t cA, double mA, double eA, DD dd_of,
+                                                 Thr thr, Nucleus& nuc) {
+  if (nw <= kWave) return cut_window_wave<1>(sh, nw, cA, mA, eA, dd_of, thr, nuc);
+  if (nw <= 2 * kWave) return cut_window_wave<2>(sh, nw, cA, mA, eA, dd_of, thr, nuc);
+  if (nw <= 4 * kWave) return cut_window_wave<4>(sh, nw, cA, mA, eA, dd_of, thr, nuc);
+  return cut_window_wave<8>(sh, nw, cA, mA, eA, dd_of, thr, nuc);
 }
 
 // cut_window for any window of at most kCap logits: a workgroup-wide
@@ -972,7 +984,7 @@ __device__ __forceinline__ bool cut_window_sub(TpShared& sh, int nw, uint32_t cA
     lo = t_lo;
     hi_ = t_hi;
   };
-  if (nc <= 512) return cut_window_wave(sh, nc, bc, bm, be, dd_of, thr_c, nuc);
+  if (nc <= 512) return cut_window_small(sh, nc, bc, bm, be, dd_of, thr_c, nuc);
   return cut_window_block(sh, nc, bc, bm, be, dd_of, thr_c, nuc);
 }
 
@@ -990,7 +1002,7 @@ template <typename DD, typename Thr>
 __device__ bool cut_window(TpShared& sh, uint32_t nw_all, uint32_t cA, double mA, double eA, DD dd_of, Thr thr,
                            Nucleus& nuc) {
   const int nw = static_cast<int>(nw_all);
-  if (nw <= 512) return cut_window_wave(sh, nw, cA, mA, eA, dd_of, thr, nuc);
+  if (nw <= 512) return cut_window_small(sh, nw, cA, mA, eA, dd_of, thr, nuc);
   return cut_window_sub(sh, nw, cA, mA, eA, dd_of, thr, nuc);
 }
 
