@@ -130,6 +130,12 @@ struct TpShared {
     double m, e, t_lo, t_hi;  // above the crossing sub-buckets; the widened thresholds
     uint32_t c, s_first, s_last;
   } sc;
+  // the window location's per-wave exchanges (each slot written once per
+  // row, so that no barrier has to follow a read)
+  struct {
+    double scan[kNW], sa[kNW], seg[kNW], d[2][kNW];
+    uint32_t u[3][kNW];
+  } loc;
 };
 
 // Calls fn(z) for every logit of the row (order irrelevant), with the
@@ -1237,17 +1243,39 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
 #pragma unroll 1
     for (int k = 0; k < kPer; ++k, w *= rho) seg += bin_mass(b0 + k, w);
   }
-  double tot = seg;
-  block_sum2(sa, tot, sh);
+  // One exchange gives the totals of sa and seg and the prefix of seg (the
+  // same sums, in the same order, as block_sum2 and block_exclusive_scan).
+  const int lane = static_cast<int>(threadIdx.x % kWave), wv = static_cast<int>(threadIdx.x / kWave);
+  double incl = seg;
+#pragma unroll
+  for (int o = 1; o < kWave; o <<= 1) {
+    const double t = __shfl_up(incl, o);
+    if (lane >= o) incl += t;
+  }
+  {
+    const double sa_w = wave_sum_d(sa), seg_w = wave_sum_d(seg);
+    if (lane == 0) {
+      sh.loc.sa[wv] = sa_w;
+      sh.loc.seg[wv] = seg_w;
+    }
+    if (lane == kWave - 1) sh.loc.scan[wv] = incl;
+    if (threadIdx.x == 0) {
+      sh.hb_lo = kHB - 1;
+      sh.hb_hi = kHB - 1;
+    }
+  }
+  __syncthreads();
+  double tot = 0.0, base = 0.0;
+  sa = 0.0;
+  for (int k = 0; k < kNW; ++k) {
+    sa += sh.loc.sa[k];
+    tot += sh.loc.seg[k];
+  }
+  for (int k = 0; k < wv; ++k) base += sh.loc.scan[k];
   tot += sa;
   const double t_lo = static_cast<double>(P) * tot * (1.0 - kWinMargin);
   const double t_hi = static_cast<double>(P) * tot * (1.0 + kWinMargin);
-  const double before = sa + block_exclusive_scan(seg, sh);
-  if (threadIdx.x == 0) {
-    sh.hb_lo = kHB - 1;
-    sh.hb_hi = kHB - 1;
-  }
-  __syncthreads();
+  const double before = sa + (base + incl - seg);
   {
     // this thread's first bins where the running mass reaches t_lo and t_hi
     int k_lo = kHB, k_hi = kHB;
@@ -1292,9 +1320,36 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
       }
     }
   }
-  W.inwin = block_sum_u(inwin, sh) + (W.b_lo < 0 ? n_above : 0u);
-  W.above = block_sum_u(above, sh) + (W.b_lo >= 0 ? n_above : 0u);  // counts are exact
-  block_sum2(sb, sb_max, sh);
+  // Sparse pass when few lanes have three buckets reaching the window: a
+  // bucket can reach it only if its maximum does (bf falls with z).
+  auto reaches = [&](float x) { return fmaf(x, hk.kz4, hk.k04) < static_cast<float>(W.b_hi + 1) * kOffQ; };
+  const bool full = reaches(tk.b3);
+  const int64_t s1 = (tk.b1v >= 0 && reaches(tk.b1)) ? tk.b1v : -1;
+  const int64_t s2 = (tk.b2v >= 0 && reaches(tk.b2)) ? tk.b2v : -1;
+  {  // one exchange for the counts, the lanes with a third bucket reaching the window and the sums below it
+    const uint32_t inwin_w = wave_sum_u(inwin), above_w = wave_sum_u(above), full_w = wave_sum_u(full ? 1u : 0u);
+    const double sb_w = wave_sum_d(sb), sbm_w = wave_sum_d(sb_max);
+    if (lane == 0) {
+      sh.loc.u[0][wv] = inwin_w;
+      sh.loc.u[1][wv] = above_w;
+      sh.loc.u[2][wv] = full_w;
+      sh.loc.d[0][wv] = sb_w;
+      sh.loc.d[1][wv] = sbm_w;
+    }
+  }
+  __syncthreads();  // also: every bin is read before the table below overwrites them
+  inwin = above = 0u;
+  uint32_t n_full = 0u;
+  sb = sb_max = 0.0;
+  for (int k = 0; k < kNW; ++k) {
+    inwin += sh.loc.u[0][k];
+    above += sh.loc.u[1][k];
+    n_full += sh.loc.u[2][k];
+    sb += sh.loc.d[0][k];
+    sb_max += sh.loc.d[1][k];
+  }
+  W.inwin = inwin + (W.b_lo < 0 ? n_above : 0u);
+  W.above = above + (W.b_lo >= 0 ? n_above : 0u);  // counts are exact
   W.s_below = sb;
   W.s_below_err = kBinMassRelErr * 1.01 * sb_max;  // 1.01: a logit's mass is below 1.0093 w_b
   if (W.inwin > static_cast<uint32_t>(kCap)) return false;
@@ -1315,13 +1370,6 @@ __device__ __forceinline__ bool hist_nucleus(const void* row, int32_t V, int64_t
   }
   __syncthreads();
 
-  // Sparse pass when few lanes have three buckets reaching the window: a
-  // bucket can reach it only if its maximum does (bf falls with z).
-  auto reaches = [&](float x) { return fmaf(x, hk.kz4, hk.k04) < static_cast<float>(W.b_hi + 1) * kOffQ; };
-  const bool full = reaches(tk.b3);
-  const int64_t s1 = (tk.b1v >= 0 && reaches(tk.b1)) ? tk.b1v : -1;
-  const int64_t s2 = (tk.b2v >= 0 && reaches(tk.b2)) ? tk.b2v : -1;
-  const uint32_t n_full = block_sum_u(full ? 1u : 0u, sh);
   if (n_full <= kSparseFullLanes &&
       exact_cut<Tin, true>(row, V, h, nvec, D, P, hk, sh, W, c0, invK, full, s1, s2, nuc))
     return true;
