@@ -86,21 +86,35 @@ __device__ __forceinline__ void tile_gemm(const float* A, int sa, const float* W
 
 // Copies ROWS x COLS floats (row-major, global) into LDS with row stride S,
 // as 16-byte vectors: every load of a thread is issued before its first
-// store, so the copy costs one memory round trip.
+// store, so the copy costs one memory round trip. stage_load and
+// stage_store are its halves, for a copy whose loads are issued early and
+// stored once the LDS is free.
+template <int ROWS, int COLS>
+struct Staged {
+  static constexpr int kVecs = ROWS * COLS / 4;
+  static_assert(kVecs % kTileThreads == 0 && COLS % 4 == 0, "whole vectors per thread");
+  f4 v[kVecs / kTileThreads];
+};
+template <int ROWS, int COLS>
+__device__ __forceinline__ void stage_load(Staged<ROWS, COLS>& st, const float* src) {
+  const f4* s4 = reinterpret_cast<const f4*>(src);
+#pragma unroll
+  for (int k = 0; k < Staged<ROWS, COLS>::kVecs / kTileThreads; ++k) st.v[k] = s4[threadIdx.x + k * kTileThreads];
+}
+template <int ROWS, int COLS, int S>
+__device__ __forceinline__ void stage_store(float* dst, const Staged<ROWS, COLS>& st) {
+  static_assert(S % 4 == 0, "rows of whole vectors");
+#pragma unroll
+  for (int k = 0; k < Staged<ROWS, COLS>::kVecs / kTileThreads; ++k) {
+    const int i = threadIdx.x + k * kTileThreads;
+    *reinterpret_cast<f4*>(dst + (i / (COLS / 4)) * S + (i % (COLS / 4)) * 4) = st.v[k];
+  }
+}
 template <int ROWS, int COLS, int S>
 __device__ __forceinline__ void stage(float* dst, const float* src) {
-  constexpr int kVecs = ROWS * COLS / 4;
-  static_assert(kVecs % kTileThreads == 0 && COLS % 4 == 0 && S % 4 == 0, "whole vectors per thread");
-  constexpr int kPer = kVecs / kTileThreads;
-  const f4* s4 = reinterpret_cast<const f4*>(src);
-  f4 v[kPer];
-#pragma unroll
-  for (int k = 0; k < kPer; ++k) v[k] = s4[threadIdx.x + k * kTileThreads];
-#pragma unroll
-  for (int k = 0; k < kPer; ++k) {
-    const int i = threadIdx.x + k * kTileThreads;
-    *reinterpret_cast<f4*>(dst + (i / (COLS / 4)) * S + (i % (COLS / 4)) * 4) = v[k];
-  }
+  Staged<ROWS, COLS> st;
+  stage_load(st, src);
+  stage_store<ROWS, COLS, S>(dst, st);
 }
 
 // The same for rows r0 .. r0+63 of a [n_rows][64] activation array (rows
@@ -123,9 +137,9 @@ __device__ __forceinline__ void stage_rows(float* dst, const float* src, int64_t
 
 // LayerNorm of the 64 values of each row held by the 16 lanes l / 16 = q of a
 // wave (4 column blocks x 4 rows per lane, MFMA layout): x[j][r] is row
-// 4q + r, column 16 j + l % 16. Biased variance, eps 1e-5.
-__device__ __forceinline__ void layer_norm_rows(f4 (&x)[4], const float* g, const float* b) {
-  const int c = threadIdx.x % 16;
+// 4q + r, column 16 j + l % 16, whose gain and bias are g[j] and b[j].
+// Biased variance, eps 1e-5.
+__device__ __forceinline__ void layer_norm_rows(f4 (&x)[4], const float (&g)[4], const float (&b)[4]) {
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     float s = x[0][r] + x[1][r] + x[2][r] + x[3][r];
@@ -142,8 +156,17 @@ __device__ __forceinline__ void layer_norm_rows(f4 (&x)[4], const float* g, cons
     for (int o = 1; o < 16; o <<= 1) v += __shfl_xor(v, o, 16);
     const float inv = 1.0f / sqrtf(v * (1.0f / D) + kLnEps);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) x[j][r] = fmaf((x[j][r] - mu) * inv, g[16 * j + c], b[16 * j + c]);
+    for (int j = 0; j < 4; ++j) x[j][r] = fmaf((x[j][r] - mu) * inv, g[j], b[j]);
   }
+}
+
+// A lane's values of NB consecutive 16-column blocks of a parameter vector
+// (column 16 j + l % 16), loaded when a kernel starts so that their latency
+// overlaps the staging.
+template <int NB>
+__device__ __forceinline__ void lane_cols(float (&out)[NB], const float* v) {
+#pragma unroll
+  for (int j = 0; j < NB; ++j) out[j] = v[16 * j + threadIdx.x % 16];
 }
 
 }  // namespace
@@ -157,6 +180,8 @@ __global__ __launch_bounds__(kTileThreads) void head_qkv_kernel(HeadArgs a, int 
   __shared__ float sW[QKV * kSA];
   const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kTile;
   const float* Wl = a.weights + kLayer0 + layer * kLayerSize;
+  float bias[QKV / 16];
+  lane_cols(bias, Wl + kB_qkv);
   if (FIRST) {
     // row position t - 1 within its request, one thread per row
     __shared__ int32_t sPos[kTile];
@@ -215,11 +240,10 @@ __global__ __launch_bounds__(kTileThreads) void head_qkv_kernel(HeadArgs a, int 
 #pragma unroll
   for (int j = 0; j < QKV / 16; ++j) {
     const int col = 16 * j + lane % 16;
-    const float bias = Wl[kB_qkv + col];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int64_t row = r0 + 16 * w + 4 * (lane / 16) + r;
-      if (row < a.n_rows) a.qkv[row * QKV + col] = acc[j][r] + bias;
+      if (row < a.n_rows) a.qkv[row * QKV + col] = acc[j][r] + bias[j];
     }
   }
 }
@@ -463,31 +487,50 @@ __global__ __launch_bounds__(kTileThreads) void head_ffn_kernel(HeadArgs a, int 
   const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kTile;
   const float* Wl = a.weights + kLayer0 + layer * kLayerSize;
   const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+  float bo[4], g1[4], be1[4], b1[FF / 16], b2[4], g2[4], be2[4];
+  lane_cols(bo, Wl + kB_o);
+  lane_cols(g1, Wl + kLn1g);
+  lane_cols(be1, Wl + kLn1b);
+  lane_cols(b1, Wl + kB_1);
+  lane_cols(b2, Wl + kB_2);
+  lane_cols(g2, Wl + kLn2g);
+  lane_cols(be2, Wl + kLn2b);
   stage_rows(sA, a.att, r0, a.n_rows);
   stage<D, D, kSA>(sW, Wl + kW_o);
-  __syncthreads();
-  // y = att W_o^T + b_o + h; h1 = LN1(y)
+  // issued now, used after the first product: W_1 and the residual rows
+  Staged<FF, D> w1;
+  stage_load(w1, Wl + kW_1);
   f4 y[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) y[j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-  tile_gemm<4, D>(sA, kSA, sW, kSA, y);
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int col = 16 * j + lane % 16;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int64_t row = r0 + 16 * w + 4 * (lane / 16) + r;
-      y[j][r] += Wl[kB_o + col] + (row < a.n_rows ? Hin[row * D + col] : 0.0f);
+      y[j][r] = row < a.n_rows ? Hin[row * D + col] : 0.0f;
     }
   }
-  layer_norm_rows(y, Wl + kLn1g, Wl + kLn1b);
+  __syncthreads();
+  // y = att W_o^T + b_o + h; h1 = LN1(y)
+  f4 p[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) p[j] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+  tile_gemm<4, D>(sA, kSA, sW, kSA, p);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) y[j][r] = p[j][r] + (bo[j] + y[j][r]);
+  }
+  layer_norm_rows(y, g1, be1);
   __syncthreads();  // everyone is done reading sA and sW
 #pragma unroll
   for (int j = 0; j < 4; ++j)
 #pragma unroll
     for (int r = 0; r < 4; ++r) sA[(16 * w + 4 * (lane / 16) + r) * kSA + 16 * j + lane % 16] = y[j][r];
-  stage<FF, D, kSA>(sW, Wl + kW_1);
+  stage_store<FF, D, kSA>(sW, w1);
   __syncthreads();
+  Staged<D, FF> w2;  // issued now, used after the second product
+  stage_load(w2, Wl + kW_2);
   // f = relu(h1 W_1^T + b_1)
   {
     f4 f[FF / 16];
@@ -497,13 +540,13 @@ __global__ __launch_bounds__(kTileThreads) void head_ffn_kernel(HeadArgs a, int 
 #pragma unroll
     for (int j = 0; j < FF / 16; ++j) {
       const int col = 16 * j + lane % 16;
-      const float bias = Wl[kB_1 + col];
+      const float bias = b1[j];
 #pragma unroll
       for (int r = 0; r < 4; ++r) sF[(16 * w + 4 * (lane / 16) + r) * kSF + col] = fmaxf(f[j][r] + bias, 0.0f);
     }
   }
   __syncthreads();  // sF complete, sW free
-  stage<D, FF, kSF>(sW, Wl + kW_2);
+  stage_store<D, FF, kSF>(sW, w2);
   __syncthreads();
   // z = f W_2^T + b_2 + h1; h2 = LN2(z)
   f4 z[4];
@@ -512,11 +555,10 @@ __global__ __launch_bounds__(kTileThreads) void head_ffn_kernel(HeadArgs a, int 
   tile_gemm<4, FF>(sF, kSF, sW, kSF, z);
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const int col = 16 * j + lane % 16;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) z[j][r] += Wl[kB_2 + col] + y[j][r];
+    for (int r = 0; r < 4; ++r) z[j][r] += b2[j] + y[j][r];
   }
-  layer_norm_rows(z, Wl + kLn2g, Wl + kLn2b);
+  layer_norm_rows(z, g2, be2);
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int col = 16 * j + lane % 16;
