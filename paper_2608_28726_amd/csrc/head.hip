@@ -66,20 +66,27 @@ __device__ int64_t request_of(const int32_t* offsets, int32_t n_req, int64_t r) 
 // C (64 x 16*NB) += A (64 x K, LDS, stride sa) x B^T, B = W (16*NB rows x K,
 // LDS, stride sw): wave w computes row block w; acc[j] is column block j in
 // the MFMA output layout (lane l, register r: row 4*(l/16) + r, column l%16
-// of the 16 x 16 block).
+// of the 16 x 16 block). The contraction runs in blocks of 16: product m =
+// 0..3 of a block takes k = k0 + 4 (l / 16) + m in lane l (any assignment
+// of a block's 16 values of k works when A and B share it), so that a lane
+// reads its four values of A and of each row of B with one 16-byte LDS
+// load. Rows start 16-byte aligned (strides of 4n floats); lanes l % 16 of
+// one k group read rows 4n floats apart, 4 banks each, without conflicts.
 template <int NB, int K>
 __device__ __forceinline__ void tile_gemm(const float* A, int sa, const float* W, int sw, f4 (&acc)[NB]) {
+  static_assert(K % 16 == 0, "blocks of 16 along the contraction");
   const int lane = threadIdx.x % kWave;
   const int w = threadIdx.x / kWave;
   const int ar = 16 * w + lane % 16;
   const int kq = lane / 16;
-#pragma unroll 4
-  for (int k0 = 0; k0 < K; k0 += 4) {
-    const float a = A[ar * sa + k0 + kq];
+#pragma unroll 2
+  for (int k0 = 0; k0 < K; k0 += 16) {
+    const f4 a4 = *reinterpret_cast<const f4*>(A + ar * sa + k0 + 4 * kq);
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-      const float b = W[(16 * j + lane % 16) * sw + k0 + kq];
-      acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, acc[j], 0, 0, 0);
+      const f4 b4 = *reinterpret_cast<const f4*>(W + (16 * j + lane % 16) * sw + k0 + 4 * kq);
+#pragma unroll
+      for (int m = 0; m < 4; ++m) acc[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(a4[m], b4[m], acc[j], 0, 0, 0);
     }
   }
 }
@@ -176,8 +183,8 @@ __device__ __forceinline__ void lane_cols(float (&out)[NB], const float* v) {
 template <bool FIRST>
 __global__ __launch_bounds__(kTileThreads) void head_qkv_kernel(HeadArgs a, int layer, const float* Hin,
                                                                float* Hout) {
-  __shared__ float sA[kTile * kSA];
-  __shared__ float sW[QKV * kSA];
+  __shared__ __attribute__((aligned(16))) float sA[kTile * kSA];
+  __shared__ __attribute__((aligned(16))) float sW[QKV * kSA];
   const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kTile;
   const float* Wl = a.weights + kLayer0 + layer * kLayerSize;
   float bias[QKV / 16];
@@ -481,9 +488,9 @@ __global__ __launch_bounds__(kPlanThreads) void head_plan_kernel(HeadArgs a) {
 // LayerNorm of a 64-row tile.
 __global__ __launch_bounds__(kTileThreads) void head_ffn_kernel(HeadArgs a, int layer, const float* Hin,
                                                                float* Hout) {
-  __shared__ float sA[kTile * kSA];   // attention output, then h1
-  __shared__ float sF[kTile * kSF];   // feed-forward hidden layer
-  __shared__ float sW[FF * kSA];      // W_o, W_1, W_2 in turn (W_2 as 64 x 128)
+  __shared__ __attribute__((aligned(16))) float sA[kTile * kSA];  // attention output, then h1
+  __shared__ __attribute__((aligned(16))) float sF[kTile * kSF];  // feed-forward hidden layer
+  __shared__ __attribute__((aligned(16))) float sW[FF * kSA];     // W_o, W_1, W_2 in turn (W_2 as 64 x 128)
   const int64_t r0 = static_cast<int64_t>(blockIdx.x) * kTile;
   const float* Wl = a.weights + kLayer0 + layer * kLayerSize;
   const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
