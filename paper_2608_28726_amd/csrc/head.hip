@@ -258,8 +258,9 @@ __global__ __launch_bounds__(kTileThreads) void head_qkv_kernel(HeadArgs a, int 
 // Scaled dot-product attention of 64 queries of one request and one head
 // over all of the request's keys, on MFMA. Each of the 4 waves takes 16
 // queries; the workgroup stages the keys and values in tiles of 64 (double
-// buffered in LDS, rows padded to 17 floats against bank conflicts; a tile's
-// loads are issued before the current tile is computed and stored after).
+// buffered in LDS, K by key and V transposed, so that a lane reads its four
+// operands of a group of products with one 16-byte load; a tile's loads are
+// issued before the current tile is computed and stored after).
 // Per group of 16 keys a wave computes the transposed scores S^T = K Q^T
 // with four v_mfma_f32_16x16x4f32 over the 16 dimensions (queries
 // pre-scaled by log2(e) / sqrt(16)), so that lane l holds the scores of
@@ -273,7 +274,11 @@ constexpr int kAttnWaves = 4;
 constexpr int kAttnQ = 16;                      // queries per wave
 constexpr int kAttnWgQ = kAttnWaves * kAttnQ;   // queries per workgroup
 constexpr int kKT = 64;                         // keys per staged tile
-constexpr int kKPad = DH + 1;                   // LDS row of one key
+// K as rows of one key and V transposed, rows of one dimension; the padding
+// keeps rows 16-byte aligned and a 16-lane group's 16-byte reads (rows 20
+// or 68 floats apart, 4 banks each) free of bank conflicts
+constexpr int kKPad = DH + 4;
+constexpr int kVPad = kKT + 4;
 #ifndef PR_ATTN_PER_CU
 #define PR_ATTN_PER_CU 2
 #endif
@@ -284,20 +289,21 @@ typedef float fx4 __attribute__((ext_vector_type(4)));
 // thread of the workgroup takes the same number of barriers; the LDS buffers
 // are free again when it returns.
 __device__ __forceinline__ void attend(const HeadArgs& a, int64_t lo, int64_t hi, int hd, int64_t q0,
-                                       float (&sK)[2][kKT * kKPad], float (&sV)[2][kKT * kKPad]) {
+                                       float (&sK)[2][kKT * kKPad], float (&sV)[2][DH * kVPad]) {
   const int64_t T = hi - lo;
   const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
   const int i16 = lane % 16, g = lane / 16;
   const int64_t qw = q0 + w * kAttnQ;  // this wave's first query
   constexpr float kScale = 1.4426950408889634f / 4.0f;  // log2(e) / sqrt(DH)
-  // B operand of S^T: Q[qw + i16][4c + g], c = 0..3
+  // B operand of S^T: Q[qw + i16][4g + c] for product c = 0..3 (each lane
+  // group g contracts over its own four consecutive dimensions)
   float qb[4];
   {
     const int64_t q = qw + i16;
     const bool ok = q < hi;
-    const float* qp = a.qkv + (ok ? q : lo) * QKV + hd * DH;
+    const f4 q4 = *reinterpret_cast<const f4*>(a.qkv + (ok ? q : lo) * QKV + hd * DH + 4 * g);
 #pragma unroll
-    for (int c = 0; c < 4; ++c) qb[c] = ok ? qp[4 * c + g] * kScale : 0.0f;
+    for (int c = 0; c < 4; ++c) qb[c] = ok ? q4[c] * kScale : 0.0f;
   }
   // One thread per (key, 4 dimensions) of a tile.
   const int kk = threadIdx.x / 4, d4 = threadIdx.x % 4;
@@ -312,16 +318,9 @@ __device__ __forceinline__ void attend(const HeadArgs& a, int64_t lo, int64_t hi
     }
   };
   auto store = [&](int buf, const f4& kv, const f4& vv) {
-    float* kd = &sK[buf][kk * kKPad + 4 * d4];
-    float* vd = &sV[buf][kk * kKPad + 4 * d4];
-    kd[0] = kv.x;
-    kd[1] = kv.y;
-    kd[2] = kv.z;
-    kd[3] = kv.w;
-    vd[0] = vv.x;
-    vd[1] = vv.y;
-    vd[2] = vv.z;
-    vd[3] = vv.w;
+    *reinterpret_cast<f4*>(&sK[buf][kk * kKPad + 4 * d4]) = kv;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) sV[buf][(4 * d4 + e) * kVPad + kk] = vv[e];
   };
   static_assert(kAttnWaves * kWave == kKT * 4, "one thread per key and 4 dimensions");
   float m = -INFINITY, l = 0.0f;  // of query i16 (the same in its 4 lanes)
@@ -342,11 +341,10 @@ __device__ __forceinline__ void attend(const HeadArgs& a, int64_t lo, int64_t hi
       fx4 st[kKT / 16];
 #pragma unroll
       for (int sub = 0; sub < kKT / 16; ++sub) {
+        const f4 k4 = *reinterpret_cast<const f4*>(&K[(sub * 16 + i16) * kKPad + 4 * g]);
         st[sub] = fx4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
-          st[sub] = __builtin_amdgcn_mfma_f32_16x16x4f32(K[(sub * 16 + i16) * kKPad + 4 * c + g], qb[c], st[sub],
-                                                         0, 0, 0);
+        for (int c = 0; c < 4; ++c) st[sub] = __builtin_amdgcn_mfma_f32_16x16x4f32(k4[c], qb[c], st[sub], 0, 0, 0);
       }
       float s[kKT / 4];
       float tm = -INFINITY;
@@ -381,10 +379,10 @@ __device__ __forceinline__ void attend(const HeadArgs& a, int64_t lo, int64_t hi
       acc.w *= __shfl(corr, 4 * g + 3);
 #pragma unroll
       for (int sub = 0; sub < kKT / 16; ++sub) {
+        // V[sub 16 + 4g + r][i16], r = 0..3: four consecutive keys of row i16 of V^T
+        const f4 v4 = *reinterpret_cast<const f4*>(&Vs[i16 * kVPad + sub * 16 + 4 * g]);
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(s[4 * sub + r], Vs[(sub * 16 + 4 * g + r) * kKPad + i16], acc,
-                                                     0, 0, 0);
+        for (int r = 0; r < 4; ++r) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(s[4 * sub + r], v4[r], acc, 0, 0, 0);
       }
     }
     if (t + 1 < ntiles) store(buf ^ 1, nk, nv);
@@ -405,8 +403,8 @@ __device__ __forceinline__ void attend(const HeadArgs& a, int64_t lo, int64_t hi
 // drew short requests take more of them. Every workgroup ends when it draws
 // an index past the item count.
 __global__ __launch_bounds__(kAttnWaves * kWave) void head_attn_kernel(HeadArgs a, int layer) {
-  __shared__ float sK[2][kKT * kKPad];
-  __shared__ float sV[2][kKT * kKPad];
+  __shared__ __attribute__((aligned(16))) float sK[2][kKT * kKPad];
+  __shared__ __attribute__((aligned(16))) float sV[2][DH * kVPad];
   __shared__ int32_t s_item;
   const int32_t n_items = a.ctl[0];
   for (;;) {
