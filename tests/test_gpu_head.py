@@ -79,6 +79,22 @@ def test_many_requests():
     assert_floats("head score (64 requests)", got[sample], ref)
 
 
+def test_thousands_of_short_requests():
+    """1,500 requests of 0..40 tokens: more requests than the planning
+    workgroup has threads, and a deep search for each row's request; every
+    score against the oracle."""
+    rng = np.random.default_rng(1500)
+    lengths = rng.integers(0, 41, 1500).tolist()
+    X, off = synthetic_sequence(lengths, 12)
+    weights = wl.head_weights(seed=9)
+    print(f"case head 1500 requests rows={X.shape[0]}", flush=True)
+    got = run_head(X, off, weights, max_len=40)
+    ref = ohead.head_scores(X.astype(np.float64), off, weights.astype(np.float64))
+    assert_floats("head score (1,500 requests)", got, ref)
+    empty = np.asarray(lengths) == 0
+    assert np.isnan(got[empty]).all() and np.isfinite(got[~empty]).all()
+
+
 def test_end_to_end_from_logits():
     """Logits -> verifier input sequence -> head -> ship, both sides from the
     logits: the oracle builds its own X."""
