@@ -273,7 +273,12 @@ __global__ __launch_bounds__(kTileThreads) void head_qkv_kernel(HeadArgs a, int 
 constexpr int kAttnWaves = 4;
 constexpr int kAttnQ = 16;                      // queries per wave
 constexpr int kAttnWgQ = kAttnWaves * kAttnQ;   // queries per workgroup
-constexpr int kKT = 64;                         // keys per staged tile
+#ifndef PR_ATTN_KT
+#define PR_ATTN_KT 64
+#endif
+constexpr int kKT = PR_ATTN_KT;                 // keys per staged tile (one softmax update)
+constexpr int kKC = kKT * 4 / (kAttnWaves * kWave);  // a thread's (key, 4 dimensions) chunks of a tile
+static_assert(kKC >= 1 && kKC * kAttnWaves * kWave == kKT * 4, "whole chunks per thread");
 // K as rows of one key and V transposed, rows of one dimension; the padding
 // keeps rows 16-byte aligned and a 16-lane group's 16-byte reads (rows 20
 // or 68 floats apart, 4 banks each) free of bank conflicts
@@ -305,29 +310,36 @@ __device__ __forceinline__ void attend(const HeadArgs& a, int64_t lo, int64_t hi
 #pragma unroll
     for (int c = 0; c < 4; ++c) qb[c] = ok ? q4[c] * kScale : 0.0f;
   }
-  // One thread per (key, 4 dimensions) of a tile.
-  const int kk = threadIdx.x / 4, d4 = threadIdx.x % 4;
-  auto load = [&](int64_t t, f4& kv, f4& vv) {
-    const int64_t key = lo + t * kKT + kk;
-    kv = f4{0.0f, 0.0f, 0.0f, 0.0f};
-    vv = kv;
-    if (key < hi) {
-      const f4* src = reinterpret_cast<const f4*>(a.qkv + key * QKV);
-      kv = src[(D + hd * DH) / 4 + d4];
-      vv = src[(2 * D + hd * DH) / 4 + d4];
+  // A thread's chunks of a tile: keys kk0 + 64 c, 4 dimensions each.
+  constexpr int kKeysPerRound = kAttnWaves * kWave / 4;
+  const int kk0 = threadIdx.x / 4, d4 = threadIdx.x % 4;
+  auto load = [&](int64_t t, f4 (&kv)[kKC], f4 (&vv)[kKC]) {
+#pragma unroll
+    for (int c = 0; c < kKC; ++c) {
+      const int64_t key = lo + t * kKT + kk0 + kKeysPerRound * c;
+      kv[c] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+      vv[c] = kv[c];
+      if (key < hi) {
+        const f4* src = reinterpret_cast<const f4*>(a.qkv + key * QKV);
+        kv[c] = src[(D + hd * DH) / 4 + d4];
+        vv[c] = src[(2 * D + hd * DH) / 4 + d4];
+      }
     }
   };
-  auto store = [&](int buf, const f4& kv, const f4& vv) {
-    *reinterpret_cast<f4*>(&sK[buf][kk * kKPad + 4 * d4]) = kv;
+  auto store = [&](int buf, const f4 (&kv)[kKC], const f4 (&vv)[kKC]) {
 #pragma unroll
-    for (int e = 0; e < 4; ++e) sV[buf][(4 * d4 + e) * kVPad + kk] = vv[e];
+    for (int c = 0; c < kKC; ++c) {
+      const int kk = kk0 + kKeysPerRound * c;
+      *reinterpret_cast<f4*>(&sK[buf][kk * kKPad + 4 * d4]) = kv[c];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) sV[buf][(4 * d4 + e) * kVPad + kk] = vv[c][e];
+    }
   };
-  static_assert(kAttnWaves * kWave == kKT * 4, "one thread per key and 4 dimensions");
   float m = -INFINITY, l = 0.0f;  // of query i16 (the same in its 4 lanes)
   fx4 acc = fx4{0.0f, 0.0f, 0.0f, 0.0f};  // O[4g + r][i16]
   const int64_t ntiles = (T + kKT - 1) / kKT;
   const bool busy = qw < hi;  // a wave whose queries all lie past the request only stages
-  f4 nk, nv;
+  f4 nk[kKC], nv[kKC];
   load(0, nk, nv);
   store(0, nk, nv);
   __syncthreads();
