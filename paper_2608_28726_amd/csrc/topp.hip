@@ -889,7 +889,7 @@ __device__ __forceinline__ bool cut_window_sub(TpShared& sh, int nw, uint32_t cA
   }
   block_max2_u(kmax, knmin, sh);  // its barriers also order the clearing before the sums
   const uint32_t hi = kmax, span = kmax - ~knmin;
-  const int shift = span < static_cast<uint32_t>(kSub) ? 0 : 24 - __clz(static_cast<int>(span));  // span >> shift < kSub
+  const int shift = span < static_cast<uint32_t>(kSub) ? 0 : 24 - __builtin_clz(span);  // span >> shift < kSub
   const double dd_hi = dd_of(key_float(hi)), dd_lo = dd_of(key_float(~knmin));
   const double mref = exp_tang(dd_hi, tab) * (1.0 + 0x1p-30);  // at least every mass of the window
   if (!(mref > 0x1p-900 && mref < 0x1p900)) return cut_window_block(sh, nw, cA, mA, eA, dd_of, thr, nuc);
