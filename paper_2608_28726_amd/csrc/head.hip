@@ -70,8 +70,9 @@ __device__ int64_t request_of(const int32_t* offsets, int32_t n_req, int64_t r) 
 // 0..3 of a block takes k = k0 + 4 (l / 16) + m in lane l (any assignment
 // of a block's 16 values of k works when A and B share it), so that a lane
 // reads its four values of A and of each row of B with one 16-byte LDS
-// load. Rows start 16-byte aligned (strides of 4n floats); lanes l % 16 of
-// one k group read rows 4n floats apart, 4 banks each, without conflicts.
+// load. Rows start 16-byte aligned; their strides (68 and 132 floats) are 4
+// modulo the 64 banks, so the 16 lanes of one k group read 16 distinct
+// groups of 4 banks.
 template <int NB, int K>
 __device__ __forceinline__ void tile_gemm(const float* A, int sa, const float* W, int sw, f4 (&acc)[NB]) {
   static_assert(K % 16 == 0, "blocks of 16 along the contraction");
