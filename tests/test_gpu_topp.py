@@ -226,6 +226,25 @@ def test_topp_large_windows(dtype):
         assert np.array_equal(g[key].view(np.uint32), g2[key].view(np.uint32)), key
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_topp_window_size_boundaries(dtype):
+    """Windows at the limits of the one-wave cut's sizes (64, 128, 256, 512
+    logits per wave, the sub-bucket cut above): a plateau of n values within
+    one bin, the rest 20 nats below, the crossing inside the plateau."""
+    V = 65536
+    rng = np.random.default_rng(640)
+    rows, ids, Ps = [], [], []
+    for n in (1, 2, 63, 64, 65, 127, 128, 129, 255, 256, 257, 511, 512, 513):
+        z = np.full(V, -20.0)
+        pos = rng.choice(V, n, replace=False)
+        z[pos] = rng.uniform(0.0, 1e-4, n)
+        rows.append(z); ids.append(int(pos[0])); Ps.append(0.5)
+    n_rows = len(rows)
+    logits, ids, T, P = _run(np.stack(rows), ids, np.ones(n_rows), Ps, dtype)
+    print(f"case topp window size boundaries {dtype}", flush=True)
+    compare_features(gpu_features(logits, ids, T, P), oracle_features(logits, ids, T, P))
+
+
 def test_topp_large_vocabulary():
     """A vocabulary of 2^20 + 3 (four times the largest workload's): random,
     flat and peaked rows against the oracle's exact cutoff."""
