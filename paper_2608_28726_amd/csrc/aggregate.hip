@@ -154,6 +154,49 @@ __device__ float radix_select(Get get, int64_t lo, int64_t n, int64_t j, uint32_
   return key_float(radix_select_keys(MemKeys<Get>{get, lo, n}, n, j, hist, sel));
 }
 
+// Sum (double), minimum, NaN presence and the j-th smallest of the wave's n
+// values get(lo + k): up to kRegKeys per lane they are read once and both
+// the statistics and the select work from registers (the sums in the order
+// of wave_stats), more are read by each.
+template <typename Get>
+__device__ float column_summary(Get get, int64_t lo, int64_t n, int64_t j, uint32_t* hist, uint32_t* sel,
+                                double& sum, float& mn, bool& has_nan) {
+  if (n > static_cast<int64_t>(kRegKeys) * kWave) {
+    wave_stats(get, lo, n, sum, mn, has_nan);
+    return key_float(radix_select_keys(MemKeys<Get>{get, lo, n}, n, j, hist, sel));
+  }
+  const int lane = threadIdx.x % kWave;
+  float v[kRegKeys];
+#pragma unroll
+  for (int r = 0; r < kRegKeys; ++r) {
+    const int64_t k = lane + static_cast<int64_t>(r) * kWave;
+    v[r] = k < n ? get(lo + k) : 0.0f;
+  }
+  double s = 0.0;
+  float m = INFINITY;
+  uint32_t nan = 0;
+  RegKeys<kRegKeys> rk;
+  rk.cnt = 0;
+#pragma unroll
+  for (int r = 0; r < kRegKeys; ++r) {
+    const bool in = lane + static_cast<int64_t>(r) * kWave < n;
+    if (in) {
+      if (v[r] != v[r]) {
+        nan = 1;
+      } else {
+        s += static_cast<double>(v[r]);
+        m = fminf(m, v[r]);
+      }
+    }
+    rk.k[r] = in ? float_key(v[r]) : 0u;
+    rk.cnt += in ? 1 : 0;
+  }
+  sum = wave_sum_d(s);
+  mn = -wave_max(-m);
+  has_nan = wave_sum_u(nan) != 0;
+  return n > 0 ? key_float(radix_select_keys(rk, n, j, hist, sel)) : 0.0f;
+}
+
 __device__ int64_t quant_rank(double q, int64_t n) {
   const double qn = q * static_cast<double>(n);
   int64_t j = static_cast<int64_t>(ceil(qn));
@@ -229,9 +272,7 @@ __global__ __launch_bounds__(kAggBlock) void aggregate_kernel(pr_token_features_
   double sum;
   float mn;
   bool nan;
-  wave_stats(get, lo, n, sum, mn, nan);
-  float q = 0.0f;
-  if (n > 0) q = radix_select(get, lo, n, quant_rank(hp.q, n), sh.hist, sh.sel);
+  const float q = column_summary(get, lo, n, n > 0 ? quant_rank(hp.q, n) : 1, sh.hist, sh.sel, sum, mn, nan);
   if (threadIdx.x % kWave == 0) {
     sh.mean_d[w] = n > 0 ? sum / static_cast<double>(n) : 0.0;
     sh.mn[w] = mn;
