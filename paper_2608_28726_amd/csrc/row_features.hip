@@ -197,9 +197,6 @@ __global__ __launch_bounds__(kWave) void row_merge_kernel(RowArgs a) {
 
 namespace {
 
-#ifndef PR_ROW_BLOCK
-#define PR_ROW_BLOCK 128
-#endif
 #ifndef PR_UNROLL_BF16
 #define PR_UNROLL_BF16 2
 #endif
@@ -215,11 +212,10 @@ namespace {
 #define PR_LOAD_DEPTH_F32 4
 #endif
 
-constexpr int kBlock = PR_ROW_BLOCK;
-// Workgroup of the plain features pass on batches of kWideRows rows or more:
-// four waves per row read the 64-request batch at 6.6 TB/s against 6.4 for
-// two (the sequence and sampling variants, whose lanes carry more state,
-// keep kBlock).
+// Workgroup of the one-row-per-workgroup tier (batches of kWideRows rows or
+// more) in every variant: four waves per row read the 64-request batch at
+// 6.6 TB/s against 6.4 for two in the plain features pass, and the sequence
+// and sampling variants gain 1-2 % as well.
 #ifndef PR_FEAT_BLOCK
 #define PR_FEAT_BLOCK 256
 #endif
@@ -319,7 +315,7 @@ static hipError_t launch_sequence_typed(const RowArgs& a, hipStream_t stream) {
   constexpr int LDW = Elem<Tin>::kVec == 8 ? PR_WIDE_LOAD_DEPTH_BF16 : PR_WIDE_LOAD_DEPTH_F32;
   const dim3 grid(static_cast<unsigned>(a.n_rows));
   if (a.n_rows >= kWideRows) {
-    row_features_kernel<Tin, kBlock, U, LD, false, true><<<grid, kBlock, 0, stream>>>(a);
+    row_features_kernel<Tin, kFeatBlock, U, LD, false, true><<<grid, kFeatBlock, 0, stream>>>(a);
   } else if (a.n_rows > 256) {
     row_features_kernel<Tin, kMidBlock, U, LDW, false, true><<<grid, kMidBlock, 0, stream>>>(a);
   } else {
@@ -342,7 +338,7 @@ static hipError_t launch_sample_typed(const RowArgs& a, hipStream_t stream) {
   constexpr int LDW = Elem<Tin>::kVec == 8 ? PR_WIDE_LOAD_DEPTH_BF16 : PR_WIDE_LOAD_DEPTH_F32;
   const dim3 grid(static_cast<unsigned>(a.n_rows));
   if (a.n_rows >= kWideRows) {
-    row_features_kernel<Tin, kBlock, U, LD, false, SEQ, true><<<grid, kBlock, 0, stream>>>(a);
+    row_features_kernel<Tin, kFeatBlock, U, LD, false, SEQ, true><<<grid, kFeatBlock, 0, stream>>>(a);
   } else if (a.n_rows > 256) {
     row_features_kernel<Tin, kMidBlock, U, LDW, false, SEQ, true><<<grid, kMidBlock, 0, stream>>>(a);
   } else {
