@@ -1511,7 +1511,8 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
   Partial p = block_merge<kTpBlock>(L, cx.c);
   const uint32_t fix = rank_fixup<Tin, kTpBlock>(row, a.V, nvec, cx);
   if constexpr (SEQ) {
-    topk::select_topk<Tin, kTpBlock, 2>(row, a.V, cx.h, 0, nvec, nvec, a.top_k, hp.b, topk_lds(sh));
+    [[clang::always_inline]] topk::select_topk<Tin, kTpBlock, 2>(row, a.V, cx.h, 0, nvec, nvec, a.top_k, hp.b,
+                                                                 topk_lds(sh));
     // the selection's scratch (the window buffer) is free again
   }
   if (threadIdx.x == 0) {
