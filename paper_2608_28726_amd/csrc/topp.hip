@@ -77,6 +77,14 @@ constexpr double kLn2D = 0.6931471805599453;    // ln(2)
 #ifndef PR_APPROX_LDX
 #define PR_APPROX_LDX 4  // loads per lane in flight in the float32 pass
 #endif
+// Loads per lane in flight in the first pass and the float32 pass: bfloat16
+// vectors hold 8 logits each, twice the registers of a float32 vector once
+// unpacked; at a depth of 4 the bfloat16 kernel spilled about 40 registers
+// and its top-p rows took 1.8 times as long.
+template <typename Tin>
+constexpr int first_pass_depth() { return sizeof(Tin) == 2 ? 2 : 4; }
+template <typename Tin>
+constexpr int approx_depth() { return sizeof(Tin) == 2 ? 2 : PR_APPROX_LDX; }
 // Relative error bound of the hardware exp2 (v_exp_f32) for arguments in
 // [-100, 1]; its largest error over every float there is 8.49e-8 (a GPU test
 // re-checks the whole range).
@@ -1152,7 +1160,7 @@ __device__ __forceinline__ bool approx_cut(const void* row, int32_t V, int64_t h
       if (slot < static_cast<uint32_t>(kCap)) sh.win[slot] = z;
     }
   };
-  for_each_logit<Tin, PR_APPROX_LDX>(row, V, h, nvec, visit);
+  for_each_logit<Tin, approx_depth<Tin>()>(row, V, h, nvec, visit);
   block_sum2(sT, tT, sh);
   block_sum2(mA, tA, sh);
   const uint32_t nw_all = sh.wcount;
@@ -1449,7 +1457,7 @@ __global__ __launch_bounds__(kTpBlock) __attribute__((amdgpu_waves_per_eu(4))) v
   const void* row = static_cast<const Tin*>(a.logits) + r * a.row_stride;
   const int64_t h = head_elems<Tin>(row, a.V);
   const int64_t nvec = (a.V - h) / VEC;
-  constexpr int kLD = 4;  // loads in flight per lane: 4 to 8 with double buffering
+  constexpr int kLD = first_pass_depth<Tin>();  // with double buffering, kLD to 2 kLD loads in flight
   vec4u v[kLD];
   stretch_prefetch<Tin, kTpBlock, kLD>(row, h, 0, nvec, v);
   const RowCtx cx = row_ctx<Tin>(a, r, row);
