@@ -20,6 +20,7 @@ spell run up to 50 % slow.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import sys
@@ -379,6 +380,11 @@ def run_offline(args, torch, pr, wl, w):
                 out = pr.route(agg["score"], w.tau)
         return out
 
+    # The collector stays off from before the spin-up to the end of the timed
+    # region: a collection pass in the timed region once held back a launch by
+    # 1.2 ms, and one between the warm-up and the timed steps idles the device.
+    gc.collect()
+    gc.disable()
     spun = spin_up(torch, wl, [b.logits for b in batches[:max(1, copies)]])
     for _ in range(args.warmup):
         step()
@@ -390,6 +396,7 @@ def run_offline(args, torch, pr, wl, w):
         step(events[k])
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    gc.enable()
     kern_times = [a.elapsed_time(b) for a, b in events]
     kern_ms = float(np.mean(kern_times))
     if sequence:  # one read of the row, id and temperature in, the 16-byte tuple out
@@ -404,6 +411,7 @@ def run_offline(args, torch, pr, wl, w):
     if n_chunks > 1:  # events bracket all chunks' row kernels and their summaries
         kernel += f" x{n_chunks} chunks (+summaries)"
     extra = {"kernel": kernel, "kernel_ms": kern_ms, "kernel_ms_median": float(np.median(kern_times)),
+             "kernel_ms_per_step": [round(float(x), 4) for x in kern_times],
              "timing": f"kernel_ms: mean over the {args.steps} timed steps of HIP events recorded around the "
                        "launch on its stream; achieved = bytes_per_launch / kernel_ms",
              "bytes_per_launch": bytes_launch,
@@ -467,10 +475,13 @@ def run_stream(args, torch, pr, wl, w):
     ref = verdicts(one_pass())  # eager pass (also clears every slot at its finish)
     # Host-paced eager pass with events around each step (per-step latency as a caller sees it).
     events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n_steps)]
+    gc.collect()
+    gc.disable()
     t0 = time.perf_counter()
     eager = verdicts(one_pass(events))
     torch.cuda.synchronize()
     eager_s = time.perf_counter() - t0
+    gc.enable()
     ks = np.array([a.elapsed_time(b) for a, b in events])
     eager_ok = same(eager, ref)
 
@@ -485,6 +496,8 @@ def run_stream(args, torch, pr, wl, w):
     with torch.cuda.graph(g):
         g_outs = one_pass()
     replays_ok = True
+    gc.collect()
+    gc.disable()
     spun = spin_up(torch, wl, [p[0] for p in pool])
     for _ in range(max(1, args.warmup)):
         g.replay()
@@ -500,6 +513,7 @@ def run_stream(args, torch, pr, wl, w):
     e1.record()
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / reps
+    gc.enable()
     pass_ms = e0.elapsed_time(e1) / reps
     replays_ok &= same(verdicts(g_outs), ref)
 
@@ -563,6 +577,8 @@ def run_calibrate(args, torch, pr, wl):
     n, q = args.pool, args.ship_fraction
     host = wl.validation_scores(n)
     s = torch.from_numpy(host).cuda()
+    gc.collect()
+    gc.disable()
     for _ in range(max(1, args.warmup)):
         tau, ns = pr.calibrate_threshold(s, q)
     torch.cuda.synchronize()
@@ -574,6 +590,7 @@ def run_calibrate(args, torch, pr, wl):
         b.record()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    gc.enable()
     call_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
     c0 = time.perf_counter()
     reps = 0

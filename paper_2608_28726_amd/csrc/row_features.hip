@@ -110,7 +110,8 @@ void row_features_kernel(RowArgs a) {
   if constexpr (SEQ) {
     __shared__ topk::Store<BLOCK> ts;
     const topk::Lds lds = ts.view();
-    topk::select_topk<Tin, BLOCK, U>(row, a.V, cx.h, vb, ve, nvec, a.top_k, seq_hook, lds);
+    // inline: out of line its LDS is reached through flat addresses
+    [[clang::always_inline]] topk::select_topk<Tin, BLOCK, U>(row, a.V, cx.h, vb, ve, nvec, a.top_k, seq_hook, lds);
     if (threadIdx.x < kWave) {  // the merged state p is valid in the first wave
       const float H = topk::topk_entropy_f32(lds.top, a.top_k, p.m, cx.c, p.S);
       const float rho = topk::position_fraction(a.offsets, a.n_req, r);
@@ -331,11 +332,15 @@ hipError_t launch_feature_sequence(const RowArgs& a, pr_dtype dtype, hipStream_t
 
 // The sampling variant: the tiers of the sequence variant, with the
 // sequence X when a.X is set.
+// Float32 rows take two vectors per step and two loads in flight here (the
+// other variants four and four): with the draw's state the float32 sampling
+// kernels had spilled up to 163 registers.
 template <typename Tin, bool SEQ>
 static hipError_t launch_sample_typed(const RowArgs& a, hipStream_t stream) {
-  constexpr int U = unroll_for<Tin>();
-  constexpr int LD = load_depth_for<Tin>();
-  constexpr int LDW = Elem<Tin>::kVec == 8 ? PR_WIDE_LOAD_DEPTH_BF16 : PR_WIDE_LOAD_DEPTH_F32;
+  constexpr bool kBf16 = Elem<Tin>::kVec == 8;
+  constexpr int U = kBf16 ? unroll_for<Tin>() : 2;  // the same with and without X: the draw depends on U
+  constexpr int LD = kBf16 ? load_depth_for<Tin>() : 2;
+  constexpr int LDW = kBf16 ? PR_WIDE_LOAD_DEPTH_BF16 : 2;
   const dim3 grid(static_cast<unsigned>(a.n_rows));
   if (a.n_rows >= kWideRows) {
     row_features_kernel<Tin, kFeatBlock, U, LD, false, SEQ, true><<<grid, kFeatBlock, 0, stream>>>(a);
